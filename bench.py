@@ -1,0 +1,241 @@
+"""Throughput of the PRCR rebinding hot path on one MI355X.
+
+A step is one pass of the whole path over one batch: position reassignment
+(prcr_reassign_coords) followed by the fused gather -> M-RoPE rebinding -> inject
+kernel (prcr_rebind_inject), both launched through the C ABI on one stream, with
+every input already resident in HBM.  Each step re-injects into the same slots,
+so every step does identical work.
+
+Default workload: 32 sequences x 256 selected tokens, 36 layers x 8 KV heads,
+head_dim 128, bf16, interleaved M-RoPE (theta 5e6), contiguous caches.  The paged
+workload (64 sequences x 512 tokens, 28 layers x 4 heads, block size 16) is
+measured in the same run and reported under "secondary".
+
+Prints one JSON line.  `value` = rebound (sequence, token, layer, KV-head)
+entries per second over the timed steps.  `roofline` is for the dominant kernel
+(prcr_rebind_inject): algorithmic bytes per launch (4 * head_dim * 2 bytes per
+entry: read K, read V, write K, write V) divided by its mean launch time from HIP
+events recorded around each launch on its own stream.  `cpu_baseline` is the
+CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+KERNEL_SOURCES = ["paper_2606_26631_amd/csrc/rebind.hip", "paper_2606_26631_amd/csrc/reassign.hip",
+                  "paper_2606_26631_amd/csrc/prcr_internal.h", "paper_2606_26631_amd/csrc/api.cpp"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def describe(w) -> dict:
+    cfg = {"workload": f"workload {w.cfg} ({w.name})", "sequences": w.B,
+           "selected_tokens": w.total_k, "layers": w.NL, "kv_heads": w.H, "head_dim": w.D,
+           "storage": w.dtype, "rope": ("interleaved" if w.interleaved else "sectioned")
+           + f" {list(w.sections)} theta {w.theta:g}", "mode": "pcr", "l_ext": 2,
+           "cache": (f"paged, block {w.block_size}, {w.n_blocks} blocks" if w.paged
+                     else f"contiguous, s_max {w.s_max}"),
+           "entries_per_step": w.entries(), "algorithmic_bytes_per_step": w.algorithmic_bytes()}
+    return cfg
+
+
+def load_counters(w, khash):
+    """HBM traffic per launch from committed rocprofv3 counter summaries, if they
+    were taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", f"counters_rebind_workload{w.cfg}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        c = json.load(f)
+    if c.get("kernel_source_hash") != khash:
+        return None
+    return c.get("traffic_bytes_per_launch")
+
+
+class Prepared:
+    def __init__(self, w, dev):
+        import numpy as np
+        import torch
+
+        import paper_2606_26631_amd as prcr
+        import workloads
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        self.w = w
+        vals = workloads.torch_values(w, dev)
+        self.mem = prcr.Memory(vals["mem_k"], vals["mem_v"], t(w.coords), t(w.n_visual))
+        self.cache = prcr.Cache(vals["cache_k"], vals["cache_v"], t(w.block_table) if w.paged else None)
+        self.rope = prcr.Rope(w.D, w.sections, w.interleaved, w.theta)
+        self.sel_off, self.sel_idx = t(w.sel_off), t(w.sel_idx)
+        self.p_txt, self.cache_len = t(w.p_txt), t(w.cache_len)
+        self.new_pos = torch.empty((w.total_k, 3), dtype=torch.float64, device=dev)
+        self.next_pos = torch.empty((w.B,), dtype=torch.int32, device=dev)
+        self.new_len = torch.empty((w.B,), dtype=torch.int32, device=dev)
+        self.slots = torch.empty((w.total_k,), dtype=torch.int64, device=dev)
+        self.err = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def reassign(self, stream):
+        import paper_2606_26631_amd as prcr
+        prcr.reassign_coords(self.mem, self.sel_off, self.sel_idx, self.p_txt, "pcr", 2,
+                             self.new_pos, self.next_pos, self.err, stream)
+
+    def rebind(self, stream):
+        import paper_2606_26631_amd as prcr
+        prcr.rebind_inject(self.rope, self.mem, self.sel_off, self.sel_idx, self.new_pos,
+                           self.cache, self.cache_len, self.new_len, self.slots, self.err, stream)
+
+
+def measure(w, steps, warmup, dev):
+    import torch
+    p = Prepared(w, dev)
+    s = torch.cuda.Stream(device=dev)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        for _ in range(warmup):
+            p.reassign(s)
+            p.rebind(s)
+        s.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+                torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(s)
+        for a, b, c in evs:
+            a.record(s)
+            p.reassign(s)
+            b.record(s)
+            p.rebind(s)
+            c.record(s)
+        t1.record(s)
+        torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    rebind_ms = [b.elapsed_time(c) for a, b, c in evs]
+    reassign_ms = [a.elapsed_time(b) for a, b, c in evs]
+    err = int(p.err.item())
+    if err != 0:
+        raise RuntimeError(f"device reported data error bits {err}")
+    del p
+    torch.cuda.empty_cache()
+    return total_ms, rebind_ms, reassign_ms
+
+
+def roofline(w, rebind_ms, traffic):
+    mean_s = sum(rebind_ms) / len(rebind_ms) / 1e3
+    gbs = w.algorithmic_bytes() / mean_s / 1e9
+    return {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "kernel": "prcr_rebind_inject", "mean_launch_us": round(mean_s * 1e6, 2),
+            "min_launch_us": round(min(rebind_ms) * 1e3, 2)}
+
+
+def cpu_baseline(w, dev, budget_s=12.0):
+    """The oracle, as it stands, on whole sequences of the workload (one sequence
+    per call: reassignment + rebind/inject into that sequence's cache), until
+    about budget_s seconds of CPU time; inputs are copied to the host untimed."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import workloads
+    vals = workloads.torch_values(w, dev)
+    done_entries, spent, seqs = 0, 0.0, 0
+    for b in range(w.B):
+        s0, s1 = int(w.sel_off[b]), int(w.sel_off[b + 1])
+        mk = workloads.as_numpy_storage(vals["mem_k"][b:b + 1])
+        mv = workloads.as_numpy_storage(vals["mem_v"][b:b + 1])
+        if w.paged:
+            used = w.block_table[b][w.block_table[b] >= 0]
+            ck = workloads.as_numpy_storage(vals["cache_k"][:, torch.from_numpy(used).long().to(dev)])
+            cv = workloads.as_numpy_storage(vals["cache_v"][:, torch.from_numpy(used).long().to(dev)])
+            table = np.arange(len(used), dtype=np.int32)[None]
+            cache = {"paged": True, "k": ck, "v": cv, "block_table": table,
+                     "block_size": w.block_size, "max_blocks": len(used), "n_blocks": len(used)}
+        else:
+            ck = workloads.as_numpy_storage(vals["cache_k"][b:b + 1])
+            cv = workloads.as_numpy_storage(vals["cache_v"][b:b + 1])
+            cache = {"paged": False, "k": ck, "v": cv, "s_max": w.s_max}
+        sel_off = np.array([0, s1 - s0])
+        sel_idx = w.sel_idx[s0:s1]
+        t = time.perf_counter()
+        pos, _, _ = oracle.reassign_batch(w.coords[b:b + 1], w.n_visual[b:b + 1], sel_off, sel_idx,
+                                          w.p_txt[b:b + 1])
+        oracle.rebind_inject(w.rope(), {"k": mk, "v": mv, "n_visual": w.n_visual[b:b + 1],
+                                        "dtype": w.dtype}, sel_off, sel_idx, pos, cache,
+                             w.cache_len[b:b + 1])
+        spent += time.perf_counter() - t
+        done_entries += (s1 - s0) * w.NL * w.H
+        seqs += 1
+        if spent >= budget_s:
+            break
+    del vals
+    torch.cuda.empty_cache()
+    return {"value": round(done_entries / spent, 1), "unit": "entries/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{seqs} of {w.B} sequences of workload {w.cfg}, one oracle call per "
+                      f"sequence ({done_entries} entries, {spent:.1f} s, numpy float64, 1 thread)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--secondary", type=int, default=5, help="second workload (0: none)")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the rebinding path shards by sequence, KV head or "
+              "layer with no exchange, and this build runs and reports N=1 only.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import workloads
+    dev = torch.device("cuda:0")
+    w = workloads.make(args.workload, "full")
+    khash = kernel_source_hash()
+    total_ms, rebind_ms, reassign_ms = measure(w, args.steps, args.warmup, dev)
+    ms_step = total_ms / args.steps
+    out = {
+        "metric": "rebound KV entries/sec (layers x heads x tokens) and achieved HBM GB/s vs peak",
+        "value": round(w.entries() * args.steps / (total_ms / 1e3), 1),
+        "unit": "entries/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": describe(w),
+        "roofline": roofline(w, rebind_ms, load_counters(w, khash)),
+        "reassign_mean_us": round(sum(reassign_ms) / len(reassign_ms) * 1e3, 2),
+        "kernel_source_hash": khash,
+    }
+    if args.secondary:
+        w2 = workloads.make(args.secondary, "full")
+        t2, r2, a2 = measure(w2, args.steps, args.warmup, dev)
+        out["secondary"] = {"config": describe(w2),
+                            "value": round(w2.entries() * args.steps / (t2 / 1e3), 1),
+                            "unit": "entries/s", "ms_per_step": round(t2 / args.steps, 4),
+                            "roofline": roofline(w2, r2, load_counters(w2, khash))}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, dev, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,219 @@
+/*
+ * prcr.h - C ABI of the MI355X (gfx950) position-rebinding cache-reuse library.
+ *
+ * Position Rebinding Cache Reuse (PRCR) revisits visual evidence during decoding
+ * without replaying visual tokens through the model (Sec. 3, Algorithm 1):
+ *
+ *   1. the raw (pre-rotary) K/V projections of every visual token are kept for
+ *      every layer together with the token's original coordinates - the Raw
+ *      Visual Evidence Memory, Eq. (6)-(7);                  -> prcr_store_raw
+ *   2. the selected tokens get new coordinates next to the current text
+ *      position - Position-Consistent Reinsertion, Eq. (8)-(10); -> prcr_reassign_coords
+ *   3. their raw keys are rotated at the new coordinates, values are reused
+ *      unchanged (Eq. (11)-(12)), and both are appended to the active decoder
+ *      cache (Eq. (13)).                                     -> prcr_rebind_inject
+ *
+ * Conventions shared by every entry point
+ *   - Every pointer inside the structs and every array argument is a DEVICE
+ *     pointer unless marked "host".  The structs themselves are host memory and
+ *     are read only during the call.
+ *   - Calls are asynchronous on `stream`.  The caller owns all buffers and keeps
+ *     them alive until the stream work completes.  The library keeps no state
+ *     between calls and allocates no memory; calls are re-entrant.
+ *   - Structural errors (null pointer, bad shape, misalignment, unsupported
+ *     combination) are detected on the host before any HIP call and returned;
+ *     nothing is launched and no output is touched.  A failed kernel launch
+ *     returns PRCR_ERR_HIP.
+ *   - Data errors found on the device (an index outside the visual-token range,
+ *     a slot beyond the cache capacity, a block-table entry outside the pool,
+ *     malformed selection offsets, a position outside the exact range) OR their
+ *     PRCR_DERR_* bit into *err_flag when err_flag is non-NULL.  The affected row
+ *     is skipped: no access ever goes out of the bounds the arguments describe.
+ *     Clear *err_flag before the call if a fresh report is wanted.
+ *   - Element types: K, V of the memory, the raw projections and the cache share
+ *     `dtype` (float32 or bfloat16).  Every K/V base pointer is 16-byte aligned,
+ *     int32 arrays 4-byte, int64 and double arrays 8-byte aligned.
+ *
+ * Layouts (row-major, innermost last)
+ *   memory K / V       [batch][max_visual][n_layers][n_kv_heads][head_dim]
+ *                      (per visual token, its per-layer K/V rows: Eq. (7)'s
+ *                      "token -> {(k, v) per layer}, coordinate" record)
+ *   memory coords      int32 [batch][max_visual][3]   original (t, h, w)
+ *   selection          CSR: sel_off int32 [batch+1] (sel_off[0] = 0,
+ *                      non-decreasing, sel_off[batch] = total_k), sel_idx int32
+ *                      [total_k]; the order inside a sequence is the injection
+ *                      order (slot cache_len[b] + j for its j-th token)
+ *   new positions      double [total_k][3]   (t, h, w)
+ *   contiguous cache   [batch][n_layers][n_kv_heads][s_max][head_dim]
+ *   paged cache        [n_layers][n_blocks][block_size][n_kv_heads][head_dim]
+ *                      with block_table int32 [batch][max_blocks]
+ *   slot_mapping       int64 [total_k]: contiguous b*s_max + slot,
+ *                      paged block*block_size + offset, -1 for a skipped row
+ */
+#ifndef PRCR_H
+#define PRCR_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum prcr_status {
+  PRCR_OK = 0,
+  PRCR_ERR_NULL = 1,          /* a required pointer is NULL                        */
+  PRCR_ERR_SHAPE = 2,         /* a size or count is out of range or inconsistent   */
+  PRCR_ERR_DTYPE = 3,         /* unknown element type                              */
+  PRCR_ERR_ALIGN = 4,         /* a pointer is not aligned as required              */
+  PRCR_ERR_MODE = 5,          /* unknown reassignment mode or negative l_ext       */
+  PRCR_ERR_UNSUPPORTED = 6,   /* no compiled kernel for this head_dim/axis map     */
+  PRCR_ERR_ALIAS = 7,         /* an output aliases an input it must not alias      */
+  PRCR_ERR_HIP = 8            /* the HIP runtime reported a launch error           */
+} prcr_status;
+
+typedef enum prcr_dtype { PRCR_F32 = 0, PRCR_BF16 = 1 } prcr_dtype;
+
+/* Reassignment rules (Sec. 3.2, Table 2). */
+typedef enum prcr_mode {
+  PRCR_MODE_PCR = 0,       /* Position-Consistent Reinsertion, Eq. (8)-(10) (default)    */
+  PRCR_MODE_SHIFT = 1,     /* region translated to start at p_txt + 1, layout kept       */
+  PRCR_MODE_IDENTITY = 2,  /* original coordinates (direct reuse, Eq. (4))               */
+  PRCR_MODE_LPA = 3,       /* Linear Position Appending: p_txt + j                       */
+  PRCR_MODE_UIR = 4        /* Uniform Interval Reinsertion: p_txt + j / (K + 1)          */
+} prcr_mode;
+
+/* Device-side data error bits (OR-ed into *err_flag). */
+#define PRCR_DERR_INDEX    1   /* selected index / source row outside its range          */
+#define PRCR_DERR_CAPACITY 2   /* slot beyond s_max or beyond max_blocks * block_size     */
+#define PRCR_DERR_BLOCK    4   /* block-table entry outside [0, n_blocks)                */
+#define PRCR_DERR_OFFSETS  8   /* sel_off not a valid CSR offset array for total_k       */
+#define PRCR_DERR_RANGE   16   /* a PCR/UIR position outside the exactly-rounded range   */
+
+/* Multimodal rotary embedding (M-RoPE).  Rotary pair i = (x_i, x_{i+head_dim/2})
+ * turns by angle p_axis(i) * theta^(-2i/head_dim).  axis(i): with
+ * interleaved = 0, t for i < section[0], h for i < section[0]+section[1], w
+ * otherwise; with interleaved = 1, h if i % 3 == 1 and i < 3*section[1], w if
+ * i % 3 == 2 and i < 3*section[2], t otherwise.  section[] sums to head_dim/2. */
+typedef struct prcr_rope {
+  int32_t head_dim;
+  int32_t section[3];
+  int32_t interleaved;
+  double theta;
+} prcr_rope;
+
+/* Raw Visual Evidence Memory, Eq. (7). */
+typedef struct prcr_mem {
+  void *k;                     /* [batch][max_visual][n_layers][n_kv_heads][head_dim] */
+  void *v;                     /* same layout                                          */
+  int32_t *coords;             /* int32 [batch][max_visual][3]                          */
+  const int32_t *n_visual;     /* int32 [batch], visual tokens stored per sequence     */
+  int32_t batch, max_visual, n_layers, n_kv_heads, head_dim;
+  prcr_dtype dtype;
+} prcr_mem;
+
+/* Active decoder cache, Eq. (13).  n_layers, n_kv_heads, head_dim and dtype are
+ * those of the memory. */
+typedef struct prcr_cache {
+  int32_t paged;               /* 0: contiguous, 1: paged                              */
+  void *k;                     /* contiguous [batch][n_layers][n_kv_heads][s_max][d]   */
+  void *v;                     /* paged [n_layers][n_blocks][block_size][n_kv_heads][d] */
+  int32_t s_max;               /* contiguous: slots per sequence                       */
+  const int32_t *block_table;  /* paged: int32 [batch][max_blocks]                     */
+  int32_t block_size, max_blocks, n_blocks;
+} prcr_cache;
+
+/*
+ * prcr_store_raw - capture one layer's pre-rotary K/V of the visual tokens
+ * into the memory (Sec. 3.1, Eq. (6)-(7)).
+ *
+ *   raw_k, raw_v  [batch][s_src][n_kv_heads][head_dim]: the layer's K/V
+ *                 projections before rotary, as the attention module makes them
+ *   vis_rows      int32 [batch][max_visual]: source row of visual token m; only
+ *                 m < n_visual[b] are read
+ *   layer         0 <= layer < n_layers
+ * Writes mem->k/v[b][m][layer] for m < n_visual[b].  A source row outside
+ * [0, s_src) is skipped with PRCR_DERR_INDEX.  mem->coords is filled by the
+ * caller (it does not depend on the layer).
+ */
+prcr_status prcr_store_raw(const prcr_mem *mem, int32_t layer,
+                           const void *raw_k, const void *raw_v, int32_t s_src,
+                           const int32_t *vis_rows, int32_t *err_flag,
+                           hipStream_t stream);
+
+/*
+ * prcr_reassign_coords - new (t, h, w) coordinates for the selected tokens and
+ * the next text position (Sec. 3.2, Eq. (8)-(10), Algorithm 1).
+ *
+ *   sel_off, sel_idx, total_k   CSR selection (see layouts); K_b =
+ *                               sel_off[b+1] - sel_off[b] may be 0
+ *   p_txt    int32 [batch]: position of the latest text token of sequence b
+ *   mode     PRCR_MODE_*; l_ext = the left extension L >= 0 (the paper uses 2)
+ *   new_pos  out double [total_k][3]
+ *   next_pos out int32 [batch]: position of the next text token
+ *
+ * PCR, per axis a over the sequence's valid selected tokens: with range
+ * [lo, hi], u = (c - lo) / (hi - lo) (u = 1/2 when hi == lo) and
+ * p = (p_txt - L) + (L + 1)(1 + (K - 1) u)/(K + 1), the exact rational rounded
+ * once to double; next_pos = p_txt + 1.  SHIFT: p = p_txt + 1 + (c - lo),
+ * next_pos = max p + 1.  IDENTITY: p = c.  LPA: p = p_txt + j (j = 1..K),
+ * next_pos = p_txt + K + 1.  UIR: p = p_txt + j/(K + 1).  A token whose index is
+ * outside [0, n_visual[b]) gets NaN positions and PRCR_DERR_INDEX and is left out
+ * of the range.  PCR/UIR positions are exact (correctly rounded) while the
+ * rational's numerator and denominator stay below 2^53; beyond that the value
+ * is within a few ulp and PRCR_DERR_RANGE is raised.
+ */
+prcr_status prcr_reassign_coords(const prcr_mem *mem,
+                                 const int32_t *sel_off, const int32_t *sel_idx,
+                                 int32_t total_k, const int32_t *p_txt,
+                                 prcr_mode mode, int32_t l_ext,
+                                 double *new_pos, int32_t *next_pos,
+                                 int32_t *err_flag, hipStream_t stream);
+
+/*
+ * prcr_rebind_inject - gather the selected memory rows for every layer and KV
+ * head (Eq. (11)), rotate the keys at new_pos and reuse the values (Eq. (12)),
+ * and append both to the active cache (Eq. (13)), all in one pass.
+ *
+ *   rope          M-RoPE definition; rope->head_dim == mem->head_dim
+ *   new_pos       double [total_k][3] (e.g. from prcr_reassign_coords)
+ *   cache_len     int32 [batch] in: first free slot of each sequence
+ *   new_cache_len int32 [batch] out (may be NULL): cache_len[b] + K_b; must
+ *                 not alias cache_len
+ *   slot_mapping  int64 [total_k] out (may be NULL)
+ *
+ * Token j of sequence b goes to slot cache_len[b] + j.  Key elements are
+ * rotated in double precision (cos/sin of the double angle) and rounded once to
+ * the storage type (round to nearest even); values are copied bit for bit.
+ * Compiled axis maps: head_dim 64 with sections [8,12,12] or interleaved
+ * [11,11,10]; head_dim 128 with [16,24,24], interleaved [22,21,21] or
+ * interleaved [24,20,20]; float32 and bfloat16; contiguous and paged.
+ */
+prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem,
+                               const int32_t *sel_off, const int32_t *sel_idx,
+                               int32_t total_k, const double *new_pos,
+                               const prcr_cache *cache, const int32_t *cache_len,
+                               int32_t *new_cache_len, int64_t *slot_mapping,
+                               int32_t *err_flag, hipStream_t stream);
+
+/* Host helpers (no GPU work). */
+
+/* Static description of a status code (host). */
+const char *prcr_status_str(prcr_status s);
+
+/* The double-precision frequencies theta^(-2i/head_dim), i < head_dim/2, that the
+ * kernels use (host; out_host holds head_dim/2 doubles). */
+prcr_status prcr_inv_freq(const prcr_rope *rope, double *out_host);
+
+/* The axis (0 = t, 1 = h, 2 = w) of each rotary pair, as the compiled kernels
+ * resolve it (host; out_host holds head_dim/2 int32). */
+prcr_status prcr_pair_axis(const prcr_rope *rope, int32_t *out_host);
+
+/* Library version as major*10000 + minor*100 + patch (host). */
+int32_t prcr_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PRCR_H */

@@ -1,0 +1,231 @@
+// extern "C" entry points: structural validation on the host, then one kernel
+// launch on the caller's stream.  No entry point allocates or keeps state.
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "prcr_internal.h"
+
+using namespace prcr;
+
+namespace {
+
+constexpr int32_t kVersion = 1 * 10000 + 0 * 100 + 0;
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int elem_bytes(prcr_dtype d) { return d == PRCR_F32 ? 4 : 2; }
+
+prcr_status check_rope(const prcr_rope *rope) {
+  if (rope == nullptr) return PRCR_ERR_NULL;
+  const int d = rope->head_dim;
+  if (d < 2 || d % 2 != 0 || d / 2 > kMaxPairs) return PRCR_ERR_SHAPE;
+  if (rope->section[0] < 0 || rope->section[1] < 0 || rope->section[2] < 0) return PRCR_ERR_SHAPE;
+  if (rope->section[0] + rope->section[1] + rope->section[2] != d / 2) return PRCR_ERR_SHAPE;
+  if (rope->interleaved != 0 && rope->interleaved != 1) return PRCR_ERR_SHAPE;
+  if (!(rope->theta > 0.0) || !std::isfinite(rope->theta)) return PRCR_ERR_SHAPE;
+  return PRCR_OK;
+}
+
+prcr_status check_mem(const prcr_mem *mem, bool need_coords) {
+  if (mem == nullptr || mem->k == nullptr || mem->v == nullptr || mem->n_visual == nullptr)
+    return PRCR_ERR_NULL;
+  if (need_coords && mem->coords == nullptr) return PRCR_ERR_NULL;
+  if (mem->dtype != PRCR_F32 && mem->dtype != PRCR_BF16) return PRCR_ERR_DTYPE;
+  if (mem->batch < 1 || mem->max_visual < 1 || mem->n_layers < 1 || mem->n_kv_heads < 1)
+    return PRCR_ERR_SHAPE;
+  const int d = mem->head_dim;
+  if (d < 2 || d % 2 != 0 || d / 2 > kMaxPairs) return PRCR_ERR_SHAPE;
+  // Each half row must be a whole number of 16-byte chunks.
+  if ((d / 2) * elem_bytes(mem->dtype) % 16 != 0) return PRCR_ERR_SHAPE;
+  if (static_cast<int64_t>(mem->n_layers) * mem->n_kv_heads > INT32_MAX / 2) return PRCR_ERR_SHAPE;
+  if (!aligned(mem->k, 16) || !aligned(mem->v, 16) || !aligned(mem->n_visual, 4))
+    return PRCR_ERR_ALIGN;
+  if (need_coords && !aligned(mem->coords, 4)) return PRCR_ERR_ALIGN;
+  return PRCR_OK;
+}
+
+prcr_status check_selection(const prcr_mem *mem, const int32_t *sel_off, const int32_t *sel_idx,
+                            int32_t total_k) {
+  if (sel_off == nullptr) return PRCR_ERR_NULL;
+  if (total_k < 0) return PRCR_ERR_SHAPE;
+  if (total_k > 0 && sel_idx == nullptr) return PRCR_ERR_NULL;
+  if (!aligned(sel_off, 4) || (sel_idx != nullptr && !aligned(sel_idx, 4))) return PRCR_ERR_ALIGN;
+  (void)mem;
+  return PRCR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *prcr_status_str(prcr_status s) {
+  switch (s) {
+    case PRCR_OK: return "ok";
+    case PRCR_ERR_NULL: return "a required pointer is NULL";
+    case PRCR_ERR_SHAPE: return "a size or count is out of range or inconsistent";
+    case PRCR_ERR_DTYPE: return "unknown element type";
+    case PRCR_ERR_ALIGN: return "a pointer is not aligned as required";
+    case PRCR_ERR_MODE: return "unknown reassignment mode or negative l_ext";
+    case PRCR_ERR_UNSUPPORTED: return "no compiled kernel for this head_dim / axis map";
+    case PRCR_ERR_ALIAS: return "an output aliases an input it must not alias";
+    case PRCR_ERR_HIP: return "HIP launch error";
+  }
+  return "unknown status";
+}
+
+int32_t prcr_version(void) { return kVersion; }
+
+prcr_status prcr_inv_freq(const prcr_rope *rope, double *out_host) {
+  const prcr_status st = check_rope(rope);
+  if (st != PRCR_OK) return st;
+  if (out_host == nullptr) return PRCR_ERR_NULL;
+  for (int i = 0; i < rope->head_dim / 2; ++i)
+    out_host[i] = std::pow(rope->theta, -(2.0 * i) / rope->head_dim);
+  return PRCR_OK;
+}
+
+prcr_status prcr_pair_axis(const prcr_rope *rope, int32_t *out_host) {
+  const prcr_status st = check_rope(rope);
+  if (st != PRCR_OK) return st;
+  if (out_host == nullptr) return PRCR_ERR_NULL;
+  const AxisMapId id = axis_map_id(*rope);
+  if (id == AxisMapId::kUnsupported) return PRCR_ERR_UNSUPPORTED;
+  for (int i = 0; i < rope->head_dim / 2; ++i) out_host[i] = axis_of_pair(id, i);
+  return PRCR_OK;
+}
+
+prcr_status prcr_store_raw(const prcr_mem *mem, int32_t layer, const void *raw_k, const void *raw_v,
+                           int32_t s_src, const int32_t *vis_rows, int32_t *err_flag,
+                           hipStream_t stream) {
+  prcr_status st = check_mem(mem, false);
+  if (st != PRCR_OK) return st;
+  if (raw_k == nullptr || raw_v == nullptr || vis_rows == nullptr) return PRCR_ERR_NULL;
+  if (layer < 0 || layer >= mem->n_layers || s_src < 1 || mem->batch > 65535) return PRCR_ERR_SHAPE;
+  if (!aligned(raw_k, 16) || !aligned(raw_v, 16) || !aligned(vis_rows, 4) ||
+      (err_flag != nullptr && !aligned(err_flag, 4)))
+    return PRCR_ERR_ALIGN;
+  StoreParams p{};
+  p.mem_k = mem->k;
+  p.mem_v = mem->v;
+  p.n_visual = mem->n_visual;
+  p.raw_k = raw_k;
+  p.raw_v = raw_v;
+  p.vis_rows = vis_rows;
+  p.err = err_flag;
+  p.batch = mem->batch;
+  p.max_visual = mem->max_visual;
+  p.n_layers = mem->n_layers;
+  p.n_kv_heads = mem->n_kv_heads;
+  p.layer = layer;
+  p.s_src = s_src;
+  p.row_bytes = mem->n_kv_heads * mem->head_dim * elem_bytes(mem->dtype);
+  return launch_store(p, stream) == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
+}
+
+prcr_status prcr_reassign_coords(const prcr_mem *mem, const int32_t *sel_off, const int32_t *sel_idx,
+                                 int32_t total_k, const int32_t *p_txt, prcr_mode mode, int32_t l_ext,
+                                 double *new_pos, int32_t *next_pos, int32_t *err_flag,
+                                 hipStream_t stream) {
+  prcr_status st = check_mem(mem, true);
+  if (st != PRCR_OK) return st;
+  st = check_selection(mem, sel_off, sel_idx, total_k);
+  if (st != PRCR_OK) return st;
+  if (p_txt == nullptr || next_pos == nullptr) return PRCR_ERR_NULL;
+  if (total_k > 0 && new_pos == nullptr) return PRCR_ERR_NULL;
+  if (mode < PRCR_MODE_PCR || mode > PRCR_MODE_UIR || l_ext < 0) return PRCR_ERR_MODE;
+  if (!aligned(p_txt, 4) || !aligned(next_pos, 4) || (new_pos != nullptr && !aligned(new_pos, 8)) ||
+      (err_flag != nullptr && !aligned(err_flag, 4)))
+    return PRCR_ERR_ALIGN;
+  ReassignParams p{};
+  p.coords = mem->coords;
+  p.n_visual = mem->n_visual;
+  p.sel_off = sel_off;
+  p.sel_idx = sel_idx;
+  p.p_txt = p_txt;
+  p.new_pos = new_pos;
+  p.next_pos = next_pos;
+  p.err = err_flag;
+  p.batch = mem->batch;
+  p.max_visual = mem->max_visual;
+  p.total_k = total_k;
+  p.mode = static_cast<int32_t>(mode);
+  p.l_ext = l_ext;
+  return launch_reassign(p, stream) == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
+}
+
+prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem, const int32_t *sel_off,
+                               const int32_t *sel_idx, int32_t total_k, const double *new_pos,
+                               const prcr_cache *cache, const int32_t *cache_len,
+                               int32_t *new_cache_len, int64_t *slot_mapping, int32_t *err_flag,
+                               hipStream_t stream) {
+  prcr_status st = check_rope(rope);
+  if (st != PRCR_OK) return st;
+  st = check_mem(mem, false);
+  if (st != PRCR_OK) return st;
+  if (rope->head_dim != mem->head_dim) return PRCR_ERR_SHAPE;
+  st = check_selection(mem, sel_off, sel_idx, total_k);
+  if (st != PRCR_OK) return st;
+  if (cache == nullptr || cache->k == nullptr || cache->v == nullptr || cache_len == nullptr)
+    return PRCR_ERR_NULL;
+  if (total_k > 0 && new_pos == nullptr) return PRCR_ERR_NULL;
+  if (cache->paged != 0 && cache->paged != 1) return PRCR_ERR_SHAPE;
+  if (cache->paged) {
+    if (cache->block_table == nullptr) return PRCR_ERR_NULL;
+    if (cache->block_size < 1 || cache->max_blocks < 1 || cache->n_blocks < 1) return PRCR_ERR_SHAPE;
+    if (!aligned(cache->block_table, 4)) return PRCR_ERR_ALIGN;
+  } else if (cache->s_max < 1) {
+    return PRCR_ERR_SHAPE;
+  }
+  if (!aligned(cache->k, 16) || !aligned(cache->v, 16) || !aligned(cache_len, 4) ||
+      (new_pos != nullptr && !aligned(new_pos, 8)) ||
+      (new_cache_len != nullptr && !aligned(new_cache_len, 4)) ||
+      (slot_mapping != nullptr && !aligned(slot_mapping, 8)) ||
+      (err_flag != nullptr && !aligned(err_flag, 4)))
+    return PRCR_ERR_ALIGN;
+  if (new_cache_len != nullptr && new_cache_len == cache_len) return PRCR_ERR_ALIAS;
+  const AxisMapId map = axis_map_id(*rope);
+  if (map == AxisMapId::kUnsupported) return PRCR_ERR_UNSUPPORTED;
+
+  RebindParams p{};
+  p.mem_k = mem->k;
+  p.mem_v = mem->v;
+  p.n_visual = mem->n_visual;
+  p.sel_off = sel_off;
+  p.sel_idx = sel_idx;
+  p.new_pos = new_pos;
+  p.cache_k = cache->k;
+  p.cache_v = cache->v;
+  p.block_table = cache->block_table;
+  p.cache_len = cache_len;
+  p.new_cache_len = new_cache_len;
+  p.slot_mapping = slot_mapping;
+  p.err = err_flag;
+  p.batch = mem->batch;
+  p.max_visual = mem->max_visual;
+  p.n_layers = mem->n_layers;
+  p.n_kv_heads = mem->n_kv_heads;
+  p.total_k = total_k;
+  p.s_max = cache->s_max;
+  p.block_size = cache->block_size;
+  p.max_blocks = cache->max_blocks;
+  p.n_blocks = cache->n_blocks;
+  // Rows of one token handled by one wavefront: a whole number of the wave's
+  // rows per iteration, at most 72 (9 iterations of 8 rows at head_dim 128).
+  const int rows_total = mem->n_layers * mem->n_kv_heads;
+  const int lanes_per_row = (mem->head_dim / 2) * elem_bytes(mem->dtype) / 16;
+  const int rows_per_iter = kWave / lanes_per_row;
+  const int max_rows = 9 * rows_per_iter;
+  const int groups = (rows_total + max_rows - 1) / max_rows;
+  int per = (rows_total + groups - 1) / groups;
+  per = (per + rows_per_iter - 1) / rows_per_iter * rows_per_iter;
+  p.rows_per_wave = per;
+  p.n_row_groups = (rows_total + per - 1) / per;
+  if (p.n_row_groups > 65535) return PRCR_ERR_SHAPE;
+  for (int i = 0; i < rope->head_dim / 2; ++i)
+    p.inv_freq[i] = std::pow(rope->theta, -(2.0 * i) / rope->head_dim);
+  const hipError_t e = launch_rebind(p, mem->dtype, mem->head_dim, map, cache->paged != 0, stream);
+  return e == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
+}
+
+}  // extern "C"

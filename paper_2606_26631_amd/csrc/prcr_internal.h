@@ -1,0 +1,104 @@
+// Internal declarations shared by the host API and the HIP kernel translation
+// units.  Not part of the public ABI.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+
+#include <hip/hip_runtime.h>
+
+#include "prcr.h"
+
+namespace prcr {
+
+constexpr int kMaxPairs = 64;        // head_dim <= 128
+constexpr int kWave = 64;            // CDNA wavefront width
+
+// ---------------------------------------------------------------------------
+// Rotary axis maps, resolved at compile time.  Pair i takes its position from
+// axis(i): 0 = t, 1 = h, 2 = w.
+// ---------------------------------------------------------------------------
+template <int ST, int SH, int SW>
+struct Sectioned {
+  static constexpr int kPairs = ST + SH + SW;
+  __host__ __device__ static constexpr int axis(int i) {
+    return i < ST ? 0 : (i < ST + SH ? 1 : 2);
+  }
+};
+
+template <int ST, int SH, int SW>
+struct Interleaved {
+  static constexpr int kPairs = ST + SH + SW;
+  __host__ __device__ static constexpr int axis(int i) {
+    return (i % 3 == 1 && i < 3 * SH) ? 1 : ((i % 3 == 2 && i < 3 * SW) ? 2 : 0);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Kernel parameter blocks (passed by value as kernel arguments).
+// ---------------------------------------------------------------------------
+struct ReassignParams {
+  const int32_t *coords;
+  const int32_t *n_visual;
+  const int32_t *sel_off;
+  const int32_t *sel_idx;
+  const int32_t *p_txt;
+  double *new_pos;
+  int32_t *next_pos;
+  int32_t *err;
+  int32_t batch, max_visual, total_k, mode, l_ext;
+};
+
+struct RebindParams {
+  const void *mem_k;
+  const void *mem_v;
+  const int32_t *n_visual;
+  const int32_t *sel_off;
+  const int32_t *sel_idx;
+  const double *new_pos;
+  void *cache_k;
+  void *cache_v;
+  const int32_t *block_table;
+  const int32_t *cache_len;
+  int32_t *new_cache_len;
+  int64_t *slot_mapping;
+  int32_t *err;
+  int32_t batch, max_visual, n_layers, n_kv_heads, total_k;
+  int32_t s_max, block_size, max_blocks, n_blocks;
+  int32_t rows_per_wave;          // rows (layer, head) of one token handled by one wave
+  int32_t n_row_groups;           // ceil(n_layers * n_kv_heads / rows_per_wave)
+  double inv_freq[kMaxPairs];     // theta^(-2i/head_dim)
+};
+
+struct StoreParams {
+  void *mem_k;
+  void *mem_v;
+  const int32_t *n_visual;
+  const void *raw_k;
+  const void *raw_v;
+  const int32_t *vis_rows;
+  int32_t *err;
+  int32_t batch, max_visual, n_layers, n_kv_heads, layer, s_src;
+  int32_t row_bytes;              // n_kv_heads * head_dim * element size
+};
+
+// Axis-map identifiers understood by the dispatcher.
+enum class AxisMapId : int {
+  kS_8_12_12 = 0,
+  kI_11_11_10 = 1,
+  kS_16_24_24 = 2,
+  kI_22_21_21 = 3,
+  kI_24_20_20 = 4,
+  kUnsupported = -1,
+};
+
+AxisMapId axis_map_id(const prcr_rope &rope);
+int axis_of_pair(AxisMapId id, int i);
+
+// Launchers (return the hipError_t of the launch).
+hipError_t launch_reassign(const ReassignParams &p, hipStream_t stream);
+hipError_t launch_rebind(const RebindParams &p, prcr_dtype dtype, int head_dim, AxisMapId map,
+                         bool paged, hipStream_t stream);
+hipError_t launch_store(const StoreParams &p, hipStream_t stream);
+
+}  // namespace prcr

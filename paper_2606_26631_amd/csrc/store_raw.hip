@@ -1,0 +1,47 @@
+// Raw Visual Evidence Memory capture (Sec. 3.1, Eq. (6)-(7)).
+//
+// For one layer, copies the pre-rotary K/V projections of every visual token
+// into the token-major memory: one wavefront per (sequence, visual token) moves
+// the token's n_kv_heads * head_dim row with 16-byte accesses.
+#include "prcr_internal.h"
+
+namespace prcr {
+namespace {
+
+constexpr int kWaves = 4;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(kWaves * kWave) void store_raw_kernel(const StoreParams p) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int m = blockIdx.x * kWaves + threadIdx.x / kWave;
+  const int b = blockIdx.y;
+  if (m >= p.max_visual || m >= p.n_visual[b]) return;
+  const int r = p.vis_rows[static_cast<int64_t>(b) * p.max_visual + m];
+  if (r < 0 || r >= p.s_src) {
+    if (lane == 0 && p.err != nullptr) atomicOr(p.err, PRCR_DERR_INDEX);
+    return;
+  }
+  const size_t src = (static_cast<size_t>(b) * p.s_src + r) * p.row_bytes;
+  const size_t dst = ((static_cast<size_t>(b) * p.max_visual + m) * p.n_layers + p.layer) * p.row_bytes;
+  const char *sk = static_cast<const char *>(p.raw_k) + src;
+  const char *sv = static_cast<const char *>(p.raw_v) + src;
+  char *dk = static_cast<char *>(p.mem_k) + dst;
+  char *dv = static_cast<char *>(p.mem_v) + dst;
+  for (int o = lane * 16; o < p.row_bytes; o += kWave * 16) {
+    const u32x4 k = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(sk + o));
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(sv + o));
+    __builtin_nontemporal_store(k, reinterpret_cast<u32x4 *>(dk + o));
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(dv + o));
+  }
+}
+
+}  // namespace
+
+hipError_t launch_store(const StoreParams &p, hipStream_t stream) {
+  const dim3 grid((p.max_visual + kWaves - 1) / kWaves, p.batch);
+  store_raw_kernel<<<grid, kWaves * kWave, 0, stream>>>(p);
+  return hipGetLastError();
+}
+
+}  // namespace prcr

@@ -1,0 +1,152 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function that
+include/prcr.h declares, and rejects malformed calls on the host before any HIP
+call (so no device work is started).  No compute call is made here."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2606_26631_amd as prcr
+from paper_2606_26631_amd.binding import CCache, CMem, CRope
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "prcr.h")
+FAKE = 0x10000          # 64 KiB-aligned placeholder address; never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(prcr_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    L = prcr.lib()
+    names = declared_functions()
+    assert {"prcr_store_raw", "prcr_reassign_coords", "prcr_rebind_inject"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in prcr.h but not exported"
+    assert L.prcr_version() == 10000
+
+
+def test_status_strings():
+    L = prcr.lib()
+    for code in range(9):
+        assert len(L.prcr_status_str(code)) > 0
+    assert L.prcr_status_str(99) == b"unknown status"
+
+
+ROPES = [(64, (8, 12, 12), False, 1e6), (64, (11, 11, 10), True, 1e6),
+         (128, (16, 24, 24), False, 1e6), (128, (22, 21, 21), True, 5e6),
+         (128, (24, 20, 20), True, 5e6)]
+
+
+@pytest.mark.parametrize("D,sections,inter,theta", ROPES)
+def test_host_tables_match_oracle(D, sections, inter, theta):
+    r = prcr.Rope(D, sections, inter, theta)
+    assert np.array_equal(np.array(r.inv_freq()), oracle.inv_freq(theta, D))
+    assert np.array_equal(np.array(r.pair_axis()), oracle.pair_axis(D, sections, inter))
+
+
+def test_unsupported_axis_map():
+    with pytest.raises(prcr.PrcrError) as e:
+        prcr.Rope(128, (32, 16, 16), False, 1e6).pair_axis()
+    assert e.value.status == 6
+
+
+# --- structural validation -------------------------------------------------
+def good():
+    rope = CRope(128, (ctypes.c_int32 * 3)(16, 24, 24), 0, 1e6)
+    mem = CMem(FAKE, FAKE, FAKE, FAKE, 2, 100, 28, 4, 128, 1)
+    cache = CCache(0, FAKE, FAKE, 512, None, 0, 0, 0)
+    return rope, mem, cache
+
+
+def call_rebind(rope, mem, cache, total_k=10, sel_off=FAKE, sel_idx=FAKE, new_pos=FAKE,
+                cache_len=FAKE, new_len=FAKE + 0x100, slots=FAKE, err=None):
+    L = prcr.lib()
+    return L.prcr_rebind_inject(ctypes.byref(rope) if rope is not None else None,
+                                ctypes.byref(mem) if mem is not None else None,
+                                sel_off, sel_idx, total_k, new_pos,
+                                ctypes.byref(cache) if cache is not None else None,
+                                cache_len, new_len, slots, err, None)
+
+
+def call_reassign(mem, mode=0, l_ext=2, total_k=10, new_pos=FAKE, p_txt=FAKE):
+    L = prcr.lib()
+    return L.prcr_reassign_coords(ctypes.byref(mem) if mem is not None else None, FAKE, FAKE,
+                                  total_k, p_txt, mode, l_ext, new_pos, FAKE, None, None)
+
+
+def call_store(mem, layer=0, raw_k=FAKE, s_src=10):
+    L = prcr.lib()
+    return L.prcr_store_raw(ctypes.byref(mem) if mem is not None else None, layer, raw_k, FAKE,
+                            s_src, FAKE, None, None)
+
+
+def test_rebind_validation_errors():
+    rope, mem, cache = good()
+    assert call_rebind(None, mem, cache) == 1
+    assert call_rebind(rope, None, cache) == 1
+    assert call_rebind(rope, mem, None) == 1
+    assert call_rebind(rope, mem, cache, sel_off=None) == 1
+    assert call_rebind(rope, mem, cache, sel_idx=None) == 1
+    assert call_rebind(rope, mem, cache, new_pos=None) == 1
+    assert call_rebind(rope, mem, cache, cache_len=None) == 1
+    assert call_rebind(rope, mem, cache, total_k=-1) == 2
+    # misaligned pointers
+    assert call_rebind(rope, mem, cache, new_pos=FAKE + 4) == 4
+    assert call_rebind(rope, mem, cache, slots=FAKE + 4) == 4
+    assert call_rebind(rope, mem, cache, sel_idx=FAKE + 2) == 4
+    # new_cache_len aliasing cache_len
+    assert call_rebind(rope, mem, cache, new_len=FAKE) == 7
+    # shapes
+    r2, m2, c2 = good(); m2.head_dim = 64
+    assert call_rebind(r2, m2, c2) == 2                # rope/mem head_dim mismatch
+    r2, m2, c2 = good(); r2.section[0] = 15
+    assert call_rebind(r2, m2, c2) == 2                # sections do not sum to d/2
+    r2, m2, c2 = good(); r2.theta = -1.0
+    assert call_rebind(r2, m2, c2) == 2
+    r2, m2, c2 = good(); r2.section[0], r2.section[1] = 32, 8
+    assert call_rebind(r2, m2, c2) == 6                # valid rope, no compiled map
+    r2, m2, c2 = good(); m2.dtype = 7
+    assert call_rebind(r2, m2, c2) == 3
+    r2, m2, c2 = good(); m2.k = FAKE + 8
+    assert call_rebind(r2, m2, c2) == 4
+    r2, m2, c2 = good(); c2.v = FAKE + 8
+    assert call_rebind(r2, m2, c2) == 4
+    r2, m2, c2 = good(); c2.s_max = 0
+    assert call_rebind(r2, m2, c2) == 2
+    r2, m2, c2 = good(); c2.paged = 1
+    assert call_rebind(r2, m2, c2) == 1                # paged without block table
+    r2, m2, c2 = good(); c2.paged, c2.block_table = 1, FAKE
+    assert call_rebind(r2, m2, c2) == 2                # paged with zero sizes
+    r2, m2, c2 = good(); c2.paged = 2
+    assert call_rebind(r2, m2, c2) == 2
+    r2, m2, c2 = good(); m2.batch = 0
+    assert call_rebind(r2, m2, c2) == 2
+
+
+def test_reassign_validation_errors():
+    _, mem, _ = good()
+    assert call_reassign(None) == 1
+    assert call_reassign(mem, mode=9) == 5
+    assert call_reassign(mem, l_ext=-1) == 5
+    assert call_reassign(mem, new_pos=None) == 1
+    assert call_reassign(mem, new_pos=FAKE + 4) == 4
+    assert call_reassign(mem, p_txt=None) == 1
+    m2 = good()[1]; m2.coords = None
+    assert call_reassign(m2) == 1
+
+
+def test_store_validation_errors():
+    _, mem, _ = good()
+    assert call_store(None) == 1
+    assert call_store(mem, layer=28) == 2
+    assert call_store(mem, layer=-1) == 2
+    assert call_store(mem, s_src=0) == 2
+    assert call_store(mem, raw_k=None) == 1
+    assert call_store(mem, raw_k=FAKE + 8) == 4

@@ -1,0 +1,211 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bit-exact: new positions, next text positions, slot mapping, new cache lengths,
+value rows and every cache byte outside the new slots.  Keys: within 1 bf16 ulp
+(bfloat16) or 1e-5 of the rotary pair's norm (float32).  Each test prints what it
+runs before touching the GPU.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_26631_amd as prcr
+import workloads
+from gpu_util import DEV, Case, assert_keys_close, assert_parity, run_both, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 5])
+def test_workload_small(cfg):
+    w = workloads.make(cfg, "small")
+    _say(f"workload {cfg} small: B={w.B} NL={w.NL} H={w.H} D={w.D} K={w.total_k}")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len)
+    exact, n = assert_parity(case, gpu, ref)
+    _say(f"  keys bit-exact {exact}/{n}")
+
+
+def test_workload2_full_size():
+    w = workloads.make(2, "full")
+    _say(f"workload 2 full: NL={w.NL} K={w.total_k}")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len)
+    exact, n = assert_parity(case, gpu, ref)
+    _say(f"  keys bit-exact {exact}/{n}")
+
+
+def test_video_four_revisits():
+    """Workload 4: four successive revisits appending to the same cache."""
+    w = workloads.make(4, "small")
+    _say(f"workload 4 small: B={w.B} NL={w.NL}, 4 revisits of 1024")
+    case = Case(w)
+    lens = w.cache_len.astype(np.int64).copy()
+    p_txt = w.p_txt.astype(np.int64).copy()
+    for r, (so, si) in enumerate(w.revisits):
+        gpu, ref = run_both(case, so, si, p_txt, lens)
+        # the GPU cache tensors are updated in place; keep the oracle's copy in step
+        assert_parity(case, gpu, ref)
+        lens = ref["new_cache_len"] + w.decode_between
+        p_txt = ref["next_pos"] + w.decode_between - 1
+        _say(f"  revisit {r} ok, next_pos {ref['next_pos'].tolist()}")
+    assert (lens <= w.s_max).all()
+
+
+@pytest.mark.parametrize("mode", ["pcr", "shift", "identity", "lpa", "uir"])
+@pytest.mark.parametrize("cfg", [1, 3])
+def test_modes(cfg, mode):
+    w = workloads.make(cfg, "small")
+    _say(f"workload {cfg} small, mode {mode}")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len, mode=mode)
+    assert_parity(case, gpu, ref)
+
+
+@pytest.mark.parametrize("l_ext", [0, 1, 5])
+def test_left_extension(l_ext):
+    w = workloads.make(5, "small")
+    _say(f"workload 5 small, L={l_ext}")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len, l_ext=l_ext)
+    assert_parity(case, gpu, ref)
+
+
+COMPILED = [
+    ("f32", 64, (8, 12, 12), False), ("f32", 64, (11, 11, 10), True),
+    ("f32", 128, (16, 24, 24), False), ("f32", 128, (22, 21, 21), True),
+    ("f32", 128, (24, 20, 20), True),
+    ("bf16", 64, (8, 12, 12), False), ("bf16", 64, (11, 11, 10), True),
+    ("bf16", 128, (16, 24, 24), False), ("bf16", 128, (22, 21, 21), True),
+    ("bf16", 128, (24, 20, 20), True),
+]
+
+
+@pytest.mark.parametrize("paged", [False, True])
+@pytest.mark.parametrize("dtype,D,sections,inter", COMPILED)
+def test_every_instantiation_with_ragged_edges(dtype, D, sections, inter, paged):
+    """Empty and one-token selections, 3 KV heads (rows not a multiple of a wave's
+    rows), a token count that leaves a partial workgroup, block size 7."""
+    w = workloads.custom(B=5, NL=3, H=3, D=D, dtype=dtype, sections=sections, interleaved=inter,
+                         theta=5e6 if inter else 1e6, frames=2, gh=9, gw=7,
+                         ks=(0, 1, 13, 0, 30), lens=(0, 11, 29, 3, 40), paged=paged, block_size=7)
+    _say(f"custom {dtype} D={D} {sections} inter={inter} paged={paged} K={w.total_k}")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len)
+    assert_parity(case, gpu, ref)
+
+
+def test_empty_selection_writes_lengths_only():
+    w = workloads.custom(B=4, ks=(0, 0, 0, 0), lens=(5, 0, 9, 2))
+    _say("all-empty selection")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len)
+    assert_parity(case, gpu, ref)
+    assert gpu["new_cache_len"].tolist() == [5, 0, 9, 2]
+
+
+def test_data_errors_are_flagged_and_skipped():
+    w = workloads.custom(B=3, NL=2, H=2, ks=(6, 4, 5), lens=(10, 25, 5), s_max=28)
+    sel_idx = w.sel_idx.copy()
+    sel_idx[2] = w.M_max + 3           # index outside the memory
+    sel_idx[3] = -1
+    _say("bad indices + capacity overflow (sequence 1 runs past s_max)")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, sel_idx, w.p_txt, w.cache_len)
+    assert ref["err"] == (oracle.ERR_INDEX | oracle.ERR_CAPACITY)
+    assert_parity(case, gpu, ref)
+
+
+def test_paged_block_errors_are_flagged_and_skipped():
+    w = workloads.custom(B=3, NL=2, H=4, ks=(6, 4, 9), lens=(10, 20, 5), paged=True,
+                         block_size=4)
+    w.block_table = w.block_table.copy()
+    w.block_table[0, 3] = w.n_blocks + 5            # slot 12..15 of sequence 0
+    w.block_table[2, -1] = -1
+    _say("paged: block id outside the pool, missing block")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len)
+    assert ref["err"] & oracle.ERR_BLOCK
+    assert_parity(case, gpu, ref)
+
+
+def test_malformed_offsets_flagged():
+    w = workloads.custom(B=3, ks=(5, 0, 3), lens=(3, 4, 5))
+    case = Case(w)
+    mem, cache = case.memory(), case.cache()
+    bad_off = to_dev(np.array([0, 5, 3, 8], np.int32))     # not non-decreasing
+    si = to_dev(w.sel_idx)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    _say("malformed sel_off")
+    pos, nxt = prcr.reassign_coords(mem, bad_off, si, to_dev(w.p_txt), err=err)
+    _, slots = prcr.rebind_inject(case.rope(), mem, bad_off, si, pos, cache, to_dev(w.cache_len),
+                                  err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) & prcr.DERR_OFFSETS
+    assert (slots.cpu().numpy() >= -1).all()
+
+
+def test_position_range_flag():
+    """A PCR rational too large for exact double division is flagged and stays close."""
+    w = workloads.custom(B=1, ks=(40,), lens=(7,), gh=12, gw=10)
+    w.coords = w.coords.copy()
+    w.coords[0, :, 1] *= 100_000_000                 # h span ~1e9
+    p_txt = np.array([2_000_000_000], np.int32)
+    case = Case(w)
+    mem = case.memory()
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    _say("huge coordinate span")
+    pos, nxt = prcr.reassign_coords(mem, to_dev(w.sel_off), to_dev(w.sel_idx), to_dev(p_txt), err=err)
+    torch.cuda.synchronize()
+    ref, nref, _ = oracle.reassign_batch(w.coords, w.n_visual, w.sel_off, w.sel_idx, p_txt)
+    assert int(err.item()) == prcr.DERR_RANGE
+    assert np.allclose(pos.cpu().numpy(), ref, rtol=4e-16, atol=0)
+    assert np.array_equal(nxt.cpu().numpy(), nref)
+
+
+def test_nondefault_stream():
+    w = workloads.make(3, "small")
+    _say("workload 3 small on a side stream")
+    case = Case(w)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream(device=DEV)
+    with torch.cuda.stream(s):
+        gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len, stream=s)
+    assert_parity(case, gpu, ref)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_store_raw(dtype):
+    B, S, NL, H, D = 3, 50, 4, 4, 128
+    M = 33
+    g = torch.Generator().manual_seed(5)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    raw_k = torch.randn((B, S, H, D), generator=g).to(tdt)
+    raw_v = torch.randn((B, S, H, D), generator=g).to(tdt)
+    rng = np.random.default_rng(5)
+    vis = np.stack([rng.choice(S, M, replace=False) for _ in range(B)]).astype(np.int32)
+    vis[1, 7] = S + 2                                   # bad source row
+    nvis = np.array([33, 20, 0], np.int32)
+    mk = torch.zeros((B, M, NL, H, D), dtype=tdt)
+    mv = torch.zeros_like(mk)
+    _say(f"store_raw {dtype}")
+    mem = prcr.Memory(mk.to(DEV), mv.to(DEV), torch.zeros((B, M, 3), dtype=torch.int32, device=DEV),
+                      to_dev(nvis))
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    for layer in range(NL):
+        prcr.store_raw(mem, layer, raw_k.to(DEV), raw_v.to(DEV), to_dev(vis), err=err)
+    torch.cuda.synchronize()
+    ek, ev = workloads.as_numpy_storage(mk), workloads.as_numpy_storage(mv)
+    hk, hv = workloads.as_numpy_storage(raw_k), workloads.as_numpy_storage(raw_v)
+    e_all = 0
+    for layer in range(NL):
+        ek, ev, e = oracle.store_raw(ek, ev, layer, hk, hv, vis, nvis)
+        e_all |= e
+    assert int(err.item()) == e_all == oracle.ERR_INDEX
+    assert np.array_equal(workloads.as_numpy_storage(mem.k), ek)
+    assert np.array_equal(workloads.as_numpy_storage(mem.v), ev)

@@ -281,3 +281,29 @@ def as_numpy_storage(t):
     if t.dtype == torch.bfloat16:
         return t.view(torch.int16).numpy().view(np.uint16)
     return t.numpy()
+
+
+def custom(B=3, NL=2, H=2, D=128, dtype="bf16", sections=(16, 24, 24), interleaved=False,
+           theta=1e6, frames=1, gh=12, gw=10, ks=(5, 0, 9), lens=(3, 40, 17), paged=False,
+           block_size=16, s_max=None, seed=7, spare_blocks=0) -> Workload:
+    """A small workload with explicit per-sequence selection sizes ``ks`` and cache
+    lengths ``lens`` (edge cases: empty and single-token selections, ragged row
+    counts, odd block sizes).  Selections are sorted random subsets of the grid."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    M = frames * gh * gw
+    coords = np.broadcast_to(_grid_coords(frames, gh, gw), (B, M, 3)).copy()
+    sels = [np.sort(rng.choice(M, size=int(k), replace=False)) for k in ks]
+    off, idx = _csr(sels)
+    lens = np.asarray(lens, dtype=np.int32)
+    kw = dict(revisits=[(off, idx)], seed=seed)
+    if paged:
+        table, max_blocks, n_blocks = _paged_tables(rng, lens, int(max(ks)), block_size)
+        if spare_blocks:
+            n_blocks += spare_blocks
+        kw.update(paged=True, block_size=block_size, block_table=table, max_blocks=max_blocks,
+                  n_blocks=n_blocks)
+    else:
+        kw.update(s_max=int(s_max if s_max is not None else int(lens.max()) + int(max(ks)) + 3))
+    return Workload(0, "custom", dtype, B, NL, H, D, M, tuple(sections), bool(interleaved),
+                    float(theta), coords, np.full(B, M, np.int32), off, idx,
+                    (lens - 1).astype(np.int32), lens, **kw)
