@@ -38,6 +38,10 @@ Readings where the paper is silent (each one is a documented choice):
 * SHIFT (second mode): p_a = (p_txt + 1) + (c_a - min_a), next = max p + 1.
 * IDENTITY (direct reuse, Eq. (4)): p = original coordinates, next = p_txt + 1.
 
+Parity unpinned: no value printed in the paper fixes the readings R1 (t axis), R2
+(degenerate axis), the SHIFT next position and R5 (LPA, UIR); their tests pin them to
+the readings above, not to the paper.
+
 Layouts (all row-major, shared with the C ABI):
   memory K/V      [B][M_max][NL][H][D]   (per visual token, its per-layer rows)
   coords          [B][M_max][3] int32    (t, h, w)

@@ -210,18 +210,6 @@ prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem, const
   p.block_size = cache->block_size;
   p.max_blocks = cache->max_blocks;
   p.n_blocks = cache->n_blocks;
-  // Rows of one token handled by one wavefront: a whole number of the wave's
-  // rows per iteration, at most 72 (9 iterations of 8 rows at head_dim 128).
-  const int rows_total = mem->n_layers * mem->n_kv_heads;
-  const int lanes_per_row = (mem->head_dim / 2) * elem_bytes(mem->dtype) / 16;
-  const int rows_per_iter = kWave / lanes_per_row;
-  const int max_rows = 9 * rows_per_iter;
-  const int groups = (rows_total + max_rows - 1) / max_rows;
-  int per = (rows_total + groups - 1) / groups;
-  per = (per + rows_per_iter - 1) / rows_per_iter * rows_per_iter;
-  p.rows_per_wave = per;
-  p.n_row_groups = (rows_total + per - 1) / per;
-  if (p.n_row_groups > 65535) return PRCR_ERR_SHAPE;
   for (int i = 0; i < rope->head_dim / 2; ++i)
     p.inv_freq[i] = std::pow(rope->theta, -(2.0 * i) / rope->head_dim);
   const hipError_t e = launch_rebind(p, mem->dtype, mem->head_dim, map, cache->paged != 0, stream);

@@ -82,12 +82,52 @@ struct Store<uint16_t> {
   }
 };
 
-template <typename T, int D, class Map, bool kPaged, int kWaves, int kUnroll>
+// Compile-time launch shape, chosen by measurement on MI355X: 4 waves per
+// workgroup, 2 row iterations in flight per wave, about 72 rows per wave, keys
+// and values in separate halves of the grid, non-temporal 16-byte accesses.
+#ifndef PRCR_WAVES_PER_BLOCK
+#define PRCR_WAVES_PER_BLOCK 4
+#endif
+#ifndef PRCR_UNROLL
+#define PRCR_UNROLL 2
+#endif
+#ifndef PRCR_ROWS_PER_WAVE
+#define PRCR_ROWS_PER_WAVE 72
+#endif
+#ifndef PRCR_SPLIT_KV
+#define PRCR_SPLIT_KV 1
+#endif
+#ifndef PRCR_NONTEMPORAL
+#define PRCR_NONTEMPORAL 1
+#endif
+
+__device__ __forceinline__ u32x4 load16(const char *p) {
+#if PRCR_NONTEMPORAL
+  return load_nt(p);
+#else
+  return *reinterpret_cast<const u32x4 *>(p);
+#endif
+}
+__device__ __forceinline__ void store16(char *p, u32x4 v) {
+#if PRCR_NONTEMPORAL
+  store_nt(p, v);
+#else
+  *reinterpret_cast<u32x4 *>(p) = v;
+#endif
+}
+
+// One wavefront = one selected token x one run of rows_per_wave (layer, head)
+// rows of it.  With kSplitKV the top of the flat workgroup index picks the
+// array: the first half rotates and stores keys, the second half copies values.
+// Workgroups are dispatched in index order, so the key half runs before the
+// value half and each wave streams one source and one destination, which
+// measured faster than moving both arrays in one wave.
+template <typename T, int D, class Map, bool kPaged, int kWaves, int kUnroll, bool kSplitKV>
 __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const RebindParams p) {
   constexpr int P = D / 2;
   constexpr int E = Store<T>::kPerChunk;   // elements per 16-byte chunk
   constexpr int LPR = P / E;               // lanes per row
-  constexpr int RPI = kWave / LPR;         // rows per wave per iteration
+  constexpr int RPI = kWave / LPR;         // rows per wave and iteration
   constexpr int kRowBytes = D * static_cast<int>(sizeof(T));
   constexpr int kHalfBytes = kRowBytes / 2;
   static_assert(Map::kPairs == P, "axis map does not match head_dim");
@@ -96,17 +136,41 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
 
+  // Flat workgroup index -> (token block, row group, K|V), token block fastest.
+  // Consecutive workgroups (which the dispatcher deals round-robin to the 8 XCDs)
+  // take consecutive tokens, so the work in flight spreads over many sequences,
+  // memory rows and cache rows at once; orders that concentrate it on fewer
+  // sequences, or give each XCD its own contiguous range, measured slower.
+  constexpr int nkv = kSplitKV ? 2 : 1;
+  const int64_t n_tblk = (static_cast<int64_t>(p.total_k) + kWaves - 1) / kWaves;
+  const int64_t n_work = n_tblk * p.n_row_groups * nkv;
+  const int64_t L = blockIdx.x;
   // New cache lengths, written once by the first workgroup (also when total_k = 0).
-  if (blockIdx.x == 0 && blockIdx.y == 0 && p.new_cache_len != nullptr) {
+  if (L == 0 && p.new_cache_len != nullptr) {
     for (int b = threadIdx.x; b < p.batch; b += blockDim.x)
       p.new_cache_len[b] = p.cache_len[b] + (p.sel_off[b + 1] - p.sel_off[b]);
   }
-
-  const int g = blockIdx.x * kWaves + wave;
+  if (L >= n_work) return;
+  const int64_t tblk = L % n_tblk;
+  const int grp = static_cast<int>((L / n_tblk) % p.n_row_groups);
+  const int kv = static_cast<int>(L / (n_tblk * p.n_row_groups));
+  const bool keys = !kSplitKV || kv == 0;
+  const bool values = !kSplitKV || kv == 1;
+  const int g = static_cast<int>(tblk * kWaves + wave);
   if (g >= p.total_k) return;
-  const int grp = blockIdx.y;
+  const int r = lane / LPR;   // this lane's row within an iteration
+  const int c = lane % LPR;   // this lane's 16-byte chunk of a half row
 
-  // Sequence of token g: (number of offsets <= g) - 1.
+  // Loads that depend only on g are issued first ...
+  const int m = p.sel_idx[g];
+  double pt = 0.0, ph = 0.0, pw = 0.0;
+  if (keys) {
+    pt = p.new_pos[3 * static_cast<int64_t>(g) + 0];
+    ph = p.new_pos[3 * static_cast<int64_t>(g) + 1];
+    pw = p.new_pos[3 * static_cast<int64_t>(g) + 2];
+  }
+  // ... then the sequence of g: (number of offsets <= g) - 1, by a ballot over
+  // the offsets held one per lane ...
   int cnt = 0;
   for (int base = 0; base <= p.batch; base += kWave) {
     const int i = base + lane;
@@ -114,139 +178,166 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
     cnt += __popcll(__ballot(le));
   }
   const int b = __builtin_amdgcn_readfirstlane(cnt - 1);
+  // ... and the per-sequence values, all at once from a clamped index.
+  const int bq = min(max(b, 0), p.batch - 1);
+  const int s0 = p.sel_off[bq];
+  const int s1 = p.sel_off[bq + 1];
+  const int nvis = p.n_visual[bq];
+  const int64_t slot = static_cast<int64_t>(p.cache_len[bq]) + (g - s0);
 
-  // Per-token validation; every lane sees the same values.
   int flags = 0;
-  int m = -1, slot = 0;
-  int64_t slot_id = -1;
-  int blk = 0, off = 0;
-  bool ok = b >= 0 && b < p.batch;
-  int s0 = 0;
-  if (ok) {
-    s0 = p.sel_off[b];
-    ok = s0 <= g && g < p.sel_off[b + 1];
-  }
+  bool ok = b >= 0 && b < p.batch && s0 <= g && g < s1;
   if (!ok) {
     flags = PRCR_DERR_OFFSETS;
-  } else {
-    m = p.sel_idx[g];
-    if (m < 0 || m >= p.n_visual[b] || m >= p.max_visual) {
-      ok = false;
-      flags = PRCR_DERR_INDEX;
-    } else {
-      const int64_t slot64 = static_cast<int64_t>(p.cache_len[b]) + (g - s0);
-      slot = static_cast<int>(slot64);
-      if constexpr (kPaged) {
-        const int64_t lb = slot64 >= 0 ? slot64 / p.block_size : -1;
-        if (lb < 0 || lb >= p.max_blocks) {
-          ok = false;
-          flags = PRCR_DERR_CAPACITY;
-        } else {
-          blk = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
-          if (blk < 0 || blk >= p.n_blocks) {
-            ok = false;
-            flags = PRCR_DERR_BLOCK;
-          } else {
-            off = static_cast<int>(slot64 - lb * p.block_size);
-            slot_id = static_cast<int64_t>(blk) * p.block_size + off;
-          }
-        }
+  } else if (m < 0 || m >= nvis || m >= p.max_visual) {
+    ok = false;
+    flags = PRCR_DERR_INDEX;
+  }
+  int64_t slot_id = -1, blk = 0, off = 0;
+  if (ok) {
+    if constexpr (kPaged) {
+      const int64_t lb = slot >= 0 ? slot / p.block_size : -1;
+      if (lb < 0 || lb >= p.max_blocks) {
+        ok = false;
+        flags = PRCR_DERR_CAPACITY;
       } else {
-        if (slot64 < 0 || slot64 >= p.s_max) {
+        blk = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
+        if (blk < 0 || blk >= p.n_blocks) {
           ok = false;
-          flags = PRCR_DERR_CAPACITY;
+          flags = PRCR_DERR_BLOCK;
         } else {
-          slot_id = static_cast<int64_t>(b) * p.s_max + slot;
+          off = slot - lb * p.block_size;
+          slot_id = blk * p.block_size + off;
         }
       }
+    } else if (slot < 0 || slot >= p.s_max) {
+      ok = false;
+      flags = PRCR_DERR_CAPACITY;
+    } else {
+      slot_id = static_cast<int64_t>(b) * p.s_max + slot;
     }
   }
-  if (grp == 0 && lane == 0) {
+  if (keys && grp == 0 && lane == 0) {
     if (p.slot_mapping != nullptr) p.slot_mapping[g] = ok ? slot_id : -1;
     if (flags != 0 && p.err != nullptr) atomicOr(p.err, flags);
   }
   if (!ok) return;
 
-  // cos/sin of this token's angles: lane i computes pair i (mod P) ...
-  const double pt = p.new_pos[3 * static_cast<int64_t>(g) + 0];
-  const double ph = p.new_pos[3 * static_cast<int64_t>(g) + 1];
-  const double pw = p.new_pos[3 * static_cast<int64_t>(g) + 2];
-  const int pair = lane % P;
-  const int ax = Map::axis(pair);
-  const double pos = ax == 0 ? pt : (ax == 1 ? ph : pw);
-  double sv, cv;
-  sincos(pos * p.inv_freq[pair], &sv, &cv);
-  // ... and lane (r, c) gathers the pairs c*E .. c*E+E-1 of its two chunks.
-  const int r = lane / LPR;
-  const int c = lane % LPR;
-  double cs[E], sn[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    cs[e] = __shfl(cv, c * E + e);
-    sn[e] = __shfl(sv, c * E + e);
-  }
-
   const int rows_total = p.n_layers * p.n_kv_heads;
   const int row0 = grp * p.rows_per_wave;
   const int row_end = min(rows_total, row0 + p.rows_per_wave);
   const size_t tok_off = (static_cast<size_t>(b) * p.max_visual + m) * rows_total;
-  const char *src_k = static_cast<const char *>(p.mem_k) + tok_off * kRowBytes + c * 16;
-  const char *src_v = static_cast<const char *>(p.mem_v) + tok_off * kRowBytes + c * 16;
-  char *dst_k = static_cast<char *>(p.cache_k) + c * 16;
-  char *dst_v = static_cast<char *>(p.cache_v) + c * 16;
-  // Destination row offset (in rows of D elements) for row index `row` of the token.
+  // Destination row offsets (in rows of head_dim elements).
   size_t dst_base;
   if constexpr (kPaged) {
     dst_base = static_cast<size_t>(blk) * p.block_size + off;   // slot within a layer's pool
   } else {
     dst_base = static_cast<size_t>(b) * rows_total;             // first (layer, head) row of b
   }
+  auto dst_offset = [&](int row) -> size_t {
+    if constexpr (kPaged) {
+      const int l = row / p.n_kv_heads;
+      const int h = row - l * p.n_kv_heads;
+      return ((static_cast<size_t>(l) * p.n_blocks * p.block_size + dst_base) * p.n_kv_heads + h) *
+             kRowBytes;
+    } else {
+      return ((dst_base + row) * p.s_max + slot) * kRowBytes;
+    }
+  };
 
-  for (int rb = row0; rb < row_end; rb += RPI * kUnroll) {
-    u32x4 kl[kUnroll], kh[kUnroll], vl[kUnroll], vh[kUnroll];
+  if (keys) {
+    // cos/sin of this token's angles: lane i computes pair i (mod P), then lane
+    // (r, c) gathers the pairs c*E .. c*E+E-1 of its two chunks by shuffles.
+    const int pair = lane % P;
+    const int ax = Map::axis(pair);
+    double sv, cv;
+    sincos((ax == 0 ? pt : (ax == 1 ? ph : pw)) * p.inv_freq[pair], &sv, &cv);
+    double cs[E], sn[E];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int row = rb + u * RPI + r;
-      if (row < row_end) {
-        const size_t o = static_cast<size_t>(row) * kRowBytes;
-        kl[u] = load_nt(src_k + o);
-        kh[u] = load_nt(src_k + o + kHalfBytes);
-        vl[u] = load_nt(src_v + o);
-        vh[u] = load_nt(src_v + o + kHalfBytes);
+    for (int e = 0; e < E; ++e) {
+      cs[e] = __shfl(cv, c * E + e);
+      sn[e] = __shfl(sv, c * E + e);
+    }
+    const char *src = static_cast<const char *>(p.mem_k) + tok_off * kRowBytes + c * 16;
+    char *dst = static_cast<char *>(p.cache_k) + c * 16;
+    for (int rb = row0; rb < row_end; rb += RPI * kUnroll) {
+      u32x4 lo[kUnroll], hi[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int row = rb + u * RPI + r;
+        if (row < row_end) {
+          lo[u] = load16(src + static_cast<size_t>(row) * kRowBytes);
+          hi[u] = load16(src + static_cast<size_t>(row) * kRowBytes + kHalfBytes);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int row = rb + u * RPI + r;
+        if (row < row_end) {
+          u32x4 ol, oh;
+          Store<T>::rotate(lo[u], hi[u], cs, sn, ol, oh);
+          const size_t d = dst_offset(row);
+          store16(dst + d, ol);
+          store16(dst + d + kHalfBytes, oh);
+        }
       }
     }
+  }
+  if (values) {
+    const char *src = static_cast<const char *>(p.mem_v) + tok_off * kRowBytes + c * 16;
+    char *dst = static_cast<char *>(p.cache_v) + c * 16;
+    for (int rb = row0; rb < row_end; rb += RPI * kUnroll) {
+      u32x4 lo[kUnroll], hi[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int row = rb + u * RPI + r;
-      if (row < row_end) {
-        size_t d;
-        if constexpr (kPaged) {
-          const int l = row / p.n_kv_heads;
-          const int h = row - l * p.n_kv_heads;
-          d = ((static_cast<size_t>(l) * p.n_blocks * p.block_size + dst_base) * p.n_kv_heads + h) *
-              kRowBytes;
-        } else {
-          d = ((dst_base + row) * p.s_max + slot) * kRowBytes;
+      for (int u = 0; u < kUnroll; ++u) {
+        const int row = rb + u * RPI + r;
+        if (row < row_end) {
+          lo[u] = load16(src + static_cast<size_t>(row) * kRowBytes);
+          hi[u] = load16(src + static_cast<size_t>(row) * kRowBytes + kHalfBytes);
         }
-        u32x4 ol, oh;
-        Store<T>::rotate(kl[u], kh[u], cs, sn, ol, oh);
-        store_nt(dst_k + d, ol);
-        store_nt(dst_k + d + kHalfBytes, oh);
-        store_nt(dst_v + d, vl[u]);
-        store_nt(dst_v + d + kHalfBytes, vh[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int row = rb + u * RPI + r;
+        if (row < row_end) {
+          const size_t d = dst_offset(row);
+          store16(dst + d, lo[u]);
+          store16(dst + d + kHalfBytes, hi[u]);
+        }
       }
     }
   }
 }
 
-constexpr int kWavesPerBlock = 4;
-constexpr int kUnrollRows = 2;
+constexpr int kWavesPerBlock = PRCR_WAVES_PER_BLOCK;
+constexpr int kUnrollRows = PRCR_UNROLL;
+constexpr bool kSplit = PRCR_SPLIT_KV != 0;
 
 template <typename T, int D, class Map, bool kPaged>
-hipError_t launch_one(const RebindParams &p, hipStream_t stream) {
-  const int bx = p.total_k > 0 ? (p.total_k + kWavesPerBlock - 1) / kWavesPerBlock : 1;
-  const dim3 grid(bx, p.n_row_groups > 0 ? p.n_row_groups : 1);
-  rebind_inject_kernel<T, D, Map, kPaged, kWavesPerBlock, kUnrollRows>
+hipError_t launch_one(const RebindParams &in, hipStream_t stream) {
+  constexpr int P = D / 2;
+  constexpr int LPR = P / Store<T>::kPerChunk;
+  constexpr int RPI = kWave / LPR;
+  RebindParams p = in;
+  // Rows of one token handled by one wave: a whole number of iterations, about
+  // PRCR_ROWS_PER_WAVE, spread evenly over the token's n_layers * n_kv_heads rows.
+  const int rows_total = p.n_layers * p.n_kv_heads;
+  const int step = RPI * kUnrollRows;
+  const int target = (PRCR_ROWS_PER_WAVE + step - 1) / step * step;
+  const int groups = (rows_total + target - 1) / target;
+  int per = (rows_total + groups - 1) / groups;
+  per = (per + step - 1) / step * step;
+  p.rows_per_wave = per;
+  p.n_row_groups = (rows_total + per - 1) / per;
+  if (p.n_row_groups > 65535) return hipErrorInvalidConfiguration;
+  // One flat grid over (token block, row group, K|V); at least one workgroup so
+  // that the new cache lengths are written when nothing is selected.
+  const int64_t n_tblk = (static_cast<int64_t>(p.total_k) + kWavesPerBlock - 1) / kWavesPerBlock;
+  int64_t n_work = n_tblk * p.n_row_groups * (kSplit ? 2 : 1);
+  if (n_work < 1) n_work = 1;
+  if (n_work > INT32_MAX) return hipErrorInvalidConfiguration;
+  const dim3 grid(static_cast<unsigned>(n_work));
+  rebind_inject_kernel<T, D, Map, kPaged, kWavesPerBlock, kUnrollRows, kSplit>
       <<<grid, kWavesPerBlock * kWave, 0, stream>>>(p);
   return hipGetLastError();
 }
