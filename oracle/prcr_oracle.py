@@ -353,11 +353,15 @@ def rebind_inject(rope: dict, mem: dict, sel_off, sel_idx, new_pos, cache: dict,
             "new_cache_len": new_len, "err": err}
 
 
-def rebind_entry(rope: dict, mem: dict, b: int, m: int, layer: int, head: int, pos):
-    """One rebound key row and its value row (storage dtype), for sampled checks."""
+def rebind_row(rope: dict, k_row, dtype: str, pos):
+    """One raw key row (storage form) rebound at pos [3]: the key half of Eq. (12)."""
     D = rope["head_dim"]
     invf = inv_freq(rope["theta"], D)
     axis = pair_axis(D, rope["sections"], rope["interleaved"])
-    x = storage_to_f64(mem["k"][b, m, layer, head], mem["dtype"])
-    y = f64_to_storage(rotate_keys(x, pos, invf, axis), mem["dtype"])
+    return f64_to_storage(rotate_keys(storage_to_f64(k_row, dtype), pos, invf, axis), dtype)
+
+
+def rebind_entry(rope: dict, mem: dict, b: int, m: int, layer: int, head: int, pos):
+    """One rebound key row and its value row (storage dtype), for sampled checks."""
+    y = rebind_row(rope, mem["k"][b, m, layer, head], mem["dtype"], pos)
     return y, np.array(mem["v"][b, m, layer, head], copy=True)
