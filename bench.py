@@ -162,6 +162,71 @@ def copy_reference(dev, nbytes=1 << 31, reps=5):
             "achieved": round(2 * nbytes / (ms / 1e3) / 1e9, 1), "unit": "GB/s"}
 
 
+def small_k_latency(dev, reps=200):
+    """Per-revisit latency at Table 3's operating points (one sequence, K = 32 and
+    128 of 768 visual tokens, Qwen3-VL-8B and -32B cache shapes), for the two-call
+    path (prcr_reassign_coords + prcr_rebind_inject) and the single fused launch
+    (prcr_revisit): once as a host loop through the Python binding, once as device
+    time per revisit with 50 revisits captured in one HIP graph."""
+    import torch
+
+    import paper_2606_26631_amd as prcr
+    import workloads
+    out = []
+    for model in ("qwen3-vl-8b", "qwen3-vl-32b"):
+        for K in (32, 128):
+            w = workloads.paper_k(model, K)
+            p = Prepared(w, dev)
+            s = torch.cuda.Stream(device=dev)
+
+            def two():
+                p.reassign(s)
+                p.rebind(s)
+
+            def fused():
+                prcr.revisit(p.rope, p.mem, p.sel_off, p.sel_idx, p.p_txt, p.cache, p.cache_len,
+                             "pcr", 2, p.new_pos, p.next_pos, p.new_len, p.slots, p.err, s)
+
+            res = {"model": model, "K": K, "entries": w.entries(), "bytes": w.algorithmic_bytes()}
+            for name, fn in (("two_launches", two), ("fused", fused)):
+                # host loop through the Python binding (bounded by host call overhead)
+                torch.cuda.synchronize()
+                with torch.cuda.stream(s):
+                    for _ in range(5):
+                        fn()
+                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    a.record(s)
+                    for _ in range(reps):
+                        fn()
+                    b.record(s)
+                    torch.cuda.synchronize()
+                res[name + "_host_loop_us"] = round(a.elapsed_time(b) / reps * 1e3, 2)
+                # device time per revisit: n_graph revisits captured in one HIP graph
+                n_graph = 50
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=s):
+                    for _ in range(n_graph):
+                        fn()
+                torch.cuda.synchronize()
+                with torch.cuda.stream(s):
+                    g.replay()
+                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    a.record(s)
+                    for _ in range(4):
+                        g.replay()
+                    b.record(s)
+                    torch.cuda.synchronize()
+                res[name + "_graph_us"] = round(a.elapsed_time(b) / (4 * n_graph) * 1e3, 2)
+                del g
+            if int(p.err.item()) != 0:
+                raise RuntimeError("device reported a data error in the small-K runs")
+            res["fused_graph_GBs"] = round(w.algorithmic_bytes() / (res["fused_graph_us"] / 1e6) / 1e9, 1)
+            out.append(res)
+            del p
+            torch.cuda.empty_cache()
+    return out
+
+
 def roofline(w, rebind_ms, traffic):
     mean_s = sum(rebind_ms) / len(rebind_ms) / 1e3
     gbs = w.algorithmic_bytes() / mean_s / 1e9
@@ -236,6 +301,7 @@ def main():
     ap.add_argument("--secondary", type=int, default=5, help="second workload (0: none)")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-small-k", action="store_true", help="skip the small-K latency section")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the rebinding path shards by sequence, KV head or "
@@ -273,6 +339,8 @@ def main():
                             "roofline": roofline(w2, r2, load_counters(w2, khash))}
         out["secondary"]["roofline"]["frac_of_copy"] = round(
             out["secondary"]["roofline"]["achieved"] / copy["achieved"], 4)
+    if not args.no_small_k:
+        out["small_k_latency"] = small_k_latency(dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, dev, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -160,7 +160,7 @@ prcr_status prcr_store_raw(const prcr_mem *mem, int32_t layer,
  * next_pos = p_txt + K + 1.  UIR: p = p_txt + j/(K + 1).  A token whose index is
  * outside [0, n_visual[b]) gets NaN positions and PRCR_DERR_INDEX and is left out
  * of the range.  PCR/UIR positions are exact (correctly rounded) while the
- * rational's numerator and denominator stay below 2^53; beyond that the value
+ * rational's numerator and denominator stay below 2^52; beyond that the value
  * is within a few ulp and PRCR_DERR_RANGE is raised.
  */
 prcr_status prcr_reassign_coords(const prcr_mem *mem,
@@ -195,6 +195,28 @@ prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem,
                                const prcr_cache *cache, const int32_t *cache_len,
                                int32_t *new_cache_len, int64_t *slot_mapping,
                                int32_t *err_flag, hipStream_t stream);
+
+/*
+ * prcr_revisit - the whole revisit in one launch: reassignment (Eq. (8)-(10),
+ * as prcr_reassign_coords) fused with gather, rebinding and injection
+ * (Eq. (11)-(13), as prcr_rebind_inject), for callers that revisit a small
+ * selection and are bound by launch latency rather than bandwidth (the paper's
+ * efficiency study uses K = 32 and 128, Table 3).
+ *
+ * Arguments are those of the two calls it replaces; new_pos is an optional
+ * output here (NULL: positions are not stored).  Results are identical to
+ * prcr_reassign_coords followed by prcr_rebind_inject.  Each wavefront reduces
+ * its own sequence's coordinate ranges, reading K_b coordinates, so for large
+ * selections (hundreds of tokens per sequence and more) the two-call path is
+ * faster.
+ */
+prcr_status prcr_revisit(const prcr_rope *rope, const prcr_mem *mem,
+                         const int32_t *sel_off, const int32_t *sel_idx, int32_t total_k,
+                         const int32_t *p_txt, prcr_mode mode, int32_t l_ext,
+                         const prcr_cache *cache, const int32_t *cache_len,
+                         double *new_pos, int32_t *next_pos,
+                         int32_t *new_cache_len, int64_t *slot_mapping,
+                         int32_t *err_flag, hipStream_t stream);
 
 /* Host helpers (no GPU work). */
 

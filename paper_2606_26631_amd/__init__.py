@@ -5,8 +5,8 @@ The work runs in hand-written HIP kernels behind the C ABI of include/prcr.h
 """
 from .binding import (DERR_BLOCK, DERR_CAPACITY, DERR_INDEX, DERR_OFFSETS, DERR_RANGE, MODES,
                       Cache, Memory, PrcrError, Rope, lib, reassign_coords, rebind_inject,
-                      store_raw)
+                      revisit, store_raw)
 
 __all__ = ["Cache", "Memory", "Rope", "PrcrError", "lib", "store_raw", "reassign_coords",
-           "rebind_inject", "MODES", "DERR_INDEX", "DERR_CAPACITY", "DERR_BLOCK", "DERR_OFFSETS",
+           "rebind_inject", "revisit", "MODES", "DERR_INDEX", "DERR_CAPACITY", "DERR_BLOCK", "DERR_OFFSETS",
            "DERR_RANGE"]

@@ -75,6 +75,10 @@ def lib() -> ctypes.CDLL:
     L.prcr_rebind_inject.argtypes = [POINTER(CRope), POINTER(CMem), c_void_p, c_void_p, c_int32,
                                      c_void_p, POINTER(CCache), c_void_p, c_void_p, c_void_p,
                                      c_void_p, c_void_p]
+    L.prcr_revisit.restype = c_int
+    L.prcr_revisit.argtypes = [POINTER(CRope), POINTER(CMem), c_void_p, c_void_p, c_int32, c_void_p,
+                               c_int, c_int32, POINTER(CCache), c_void_p, c_void_p, c_void_p,
+                               c_void_p, c_void_p, c_void_p, c_void_p]
     _LIB = L
     return L
 
@@ -304,3 +308,48 @@ def rebind_inject(rope: Rope, mem: Memory, sel_off, sel_idx, new_pos, cache: Cac
                                   _stream(stream, mem.device))
     _check("prcr_rebind_inject", st)
     return new_cache_len, slot_mapping
+
+
+def revisit(rope: Rope, mem: Memory, sel_off, sel_idx, p_txt, cache: Cache, cache_len,
+            mode: str = "pcr", l_ext: int = 2, new_pos=None, next_pos=None, new_cache_len=None,
+            slot_mapping=None, err=None, stream=None, store_positions: bool = True):
+    """Reassignment + rebinding + injection in one launch (prcr_revisit).
+
+    Returns (new_pos or None, next_pos, new_cache_len, slot_mapping)."""
+    torch = _torch()
+    total_k = _selection(mem, sel_off, sel_idx)
+    B = mem.k.shape[0]
+    cache.check_matches(mem)
+    _need(p_txt, "p_txt", torch.int32, 1, mem.device)
+    _need(cache_len, "cache_len", torch.int32, 1, mem.device)
+    _shape(p_txt, "p_txt", (B,))
+    _shape(cache_len, "cache_len", (B,))
+    if new_pos is None and store_positions:
+        new_pos = torch.empty((total_k, 3), dtype=torch.float64, device=mem.device)
+    if new_pos is not None:
+        _need(new_pos, "new_pos", torch.float64, 2, mem.device)
+        _shape(new_pos, "new_pos", (total_k, 3))
+    if next_pos is None:
+        next_pos = torch.empty((B,), dtype=torch.int32, device=mem.device)
+    if new_cache_len is None:
+        new_cache_len = torch.empty((B,), dtype=torch.int32, device=mem.device)
+    if slot_mapping is None:
+        slot_mapping = torch.empty((total_k,), dtype=torch.int64, device=mem.device)
+    _need(next_pos, "next_pos", torch.int32, 1, mem.device)
+    _need(new_cache_len, "new_cache_len", torch.int32, 1, mem.device)
+    _need(slot_mapping, "slot_mapping", torch.int64, 1, mem.device)
+    _shape(next_pos, "next_pos", (B,))
+    _shape(new_cache_len, "new_cache_len", (B,))
+    _shape(slot_mapping, "slot_mapping", (total_k,))
+    if new_cache_len.data_ptr() == cache_len.data_ptr():
+        raise ValueError("new_cache_len must not alias cache_len")
+    _err(err, mem.device)
+    if mode not in MODES:
+        raise ValueError(f"mode must be one of {sorted(MODES)}")
+    st = lib().prcr_revisit(ctypes.byref(rope.to_c()), ctypes.byref(mem.to_c()), _ptr(sel_off),
+                            _ptr(sel_idx), total_k, _ptr(p_txt), MODES[mode], int(l_ext),
+                            ctypes.byref(cache.to_c()), _ptr(cache_len), _ptr(new_pos),
+                            _ptr(next_pos), _ptr(new_cache_len), _ptr(slot_mapping), _ptr(err),
+                            _stream(stream, mem.device))
+    _check("prcr_revisit", st)
+    return new_pos, next_pos, new_cache_len, slot_mapping

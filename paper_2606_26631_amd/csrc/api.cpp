@@ -154,21 +154,24 @@ prcr_status prcr_reassign_coords(const prcr_mem *mem, const int32_t *sel_off, co
   return launch_reassign(p, stream) == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
 }
 
-prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem, const int32_t *sel_off,
-                               const int32_t *sel_idx, int32_t total_k, const double *new_pos,
-                               const prcr_cache *cache, const int32_t *cache_len,
-                               int32_t *new_cache_len, int64_t *slot_mapping, int32_t *err_flag,
-                               hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared checks and parameter block of prcr_rebind_inject and prcr_revisit.
+prcr_status prepare_rebind(const prcr_rope *rope, const prcr_mem *mem, const int32_t *sel_off,
+                           const int32_t *sel_idx, int32_t total_k, const prcr_cache *cache,
+                           const int32_t *cache_len, int32_t *new_cache_len, int64_t *slot_mapping,
+                           int32_t *err_flag, bool need_coords, RebindParams *out, AxisMapId *map) {
   prcr_status st = check_rope(rope);
   if (st != PRCR_OK) return st;
-  st = check_mem(mem, false);
+  st = check_mem(mem, need_coords);
   if (st != PRCR_OK) return st;
   if (rope->head_dim != mem->head_dim) return PRCR_ERR_SHAPE;
   st = check_selection(mem, sel_off, sel_idx, total_k);
   if (st != PRCR_OK) return st;
   if (cache == nullptr || cache->k == nullptr || cache->v == nullptr || cache_len == nullptr)
     return PRCR_ERR_NULL;
-  if (total_k > 0 && new_pos == nullptr) return PRCR_ERR_NULL;
   if (cache->paged != 0 && cache->paged != 1) return PRCR_ERR_SHAPE;
   if (cache->paged) {
     if (cache->block_table == nullptr) return PRCR_ERR_NULL;
@@ -178,22 +181,21 @@ prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem, const
     return PRCR_ERR_SHAPE;
   }
   if (!aligned(cache->k, 16) || !aligned(cache->v, 16) || !aligned(cache_len, 4) ||
-      (new_pos != nullptr && !aligned(new_pos, 8)) ||
       (new_cache_len != nullptr && !aligned(new_cache_len, 4)) ||
       (slot_mapping != nullptr && !aligned(slot_mapping, 8)) ||
       (err_flag != nullptr && !aligned(err_flag, 4)))
     return PRCR_ERR_ALIGN;
   if (new_cache_len != nullptr && new_cache_len == cache_len) return PRCR_ERR_ALIAS;
-  const AxisMapId map = axis_map_id(*rope);
-  if (map == AxisMapId::kUnsupported) return PRCR_ERR_UNSUPPORTED;
+  *map = axis_map_id(*rope);
+  if (*map == AxisMapId::kUnsupported) return PRCR_ERR_UNSUPPORTED;
 
-  RebindParams p{};
+  RebindParams &p = *out;
+  p = RebindParams{};
   p.mem_k = mem->k;
   p.mem_v = mem->v;
   p.n_visual = mem->n_visual;
   p.sel_off = sel_off;
   p.sel_idx = sel_idx;
-  p.new_pos = new_pos;
   p.cache_k = cache->k;
   p.cache_v = cache->v;
   p.block_table = cache->block_table;
@@ -212,7 +214,52 @@ prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem, const
   p.n_blocks = cache->n_blocks;
   for (int i = 0; i < rope->head_dim / 2; ++i)
     p.inv_freq[i] = std::pow(rope->theta, -(2.0 * i) / rope->head_dim);
-  const hipError_t e = launch_rebind(p, mem->dtype, mem->head_dim, map, cache->paged != 0, stream);
+  return PRCR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem, const int32_t *sel_off,
+                               const int32_t *sel_idx, int32_t total_k, const double *new_pos,
+                               const prcr_cache *cache, const int32_t *cache_len,
+                               int32_t *new_cache_len, int64_t *slot_mapping, int32_t *err_flag,
+                               hipStream_t stream) {
+  RebindParams p;
+  AxisMapId map;
+  const prcr_status st = prepare_rebind(rope, mem, sel_off, sel_idx, total_k, cache, cache_len,
+                                        new_cache_len, slot_mapping, err_flag, false, &p, &map);
+  if (st != PRCR_OK) return st;
+  if (total_k > 0 && new_pos == nullptr) return PRCR_ERR_NULL;
+  if (new_pos != nullptr && !aligned(new_pos, 8)) return PRCR_ERR_ALIGN;
+  p.new_pos = new_pos;
+  const hipError_t e = launch_rebind(p, mem->dtype, mem->head_dim, map, cache->paged != 0, false, stream);
+  return e == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
+}
+
+prcr_status prcr_revisit(const prcr_rope *rope, const prcr_mem *mem, const int32_t *sel_off,
+                         const int32_t *sel_idx, int32_t total_k, const int32_t *p_txt,
+                         prcr_mode mode, int32_t l_ext, const prcr_cache *cache,
+                         const int32_t *cache_len, double *new_pos, int32_t *next_pos,
+                         int32_t *new_cache_len, int64_t *slot_mapping, int32_t *err_flag,
+                         hipStream_t stream) {
+  RebindParams p;
+  AxisMapId map;
+  const prcr_status st = prepare_rebind(rope, mem, sel_off, sel_idx, total_k, cache, cache_len,
+                                        new_cache_len, slot_mapping, err_flag, true, &p, &map);
+  if (st != PRCR_OK) return st;
+  if (p_txt == nullptr || next_pos == nullptr) return PRCR_ERR_NULL;
+  if (mode < PRCR_MODE_PCR || mode > PRCR_MODE_UIR || l_ext < 0) return PRCR_ERR_MODE;
+  if (!aligned(p_txt, 4) || !aligned(next_pos, 4) || (new_pos != nullptr && !aligned(new_pos, 8)))
+    return PRCR_ERR_ALIGN;
+  p.coords = mem->coords;
+  p.p_txt = p_txt;
+  p.pos_out = new_pos;
+  p.next_pos = next_pos;
+  p.mode = static_cast<int32_t>(mode);
+  p.l_ext = l_ext;
+  const hipError_t e = launch_rebind(p, mem->dtype, mem->head_dim, map, cache->paged != 0, true, stream);
   return e == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
 }
 

@@ -67,6 +67,12 @@ struct RebindParams {
   int32_t s_max, block_size, max_blocks, n_blocks;
   int32_t rows_per_wave;          // rows (layer, head) of one token handled by one wave
   int32_t n_row_groups;           // ceil(n_layers * n_kv_heads / rows_per_wave)
+  // Fused revisit only (positions computed in the kernel instead of read):
+  const int32_t *coords;          // [batch][max_visual][3]
+  const int32_t *p_txt;           // [batch]
+  double *pos_out;                // [total_k][3] or null
+  int32_t *next_pos;              // [batch]
+  int32_t mode, l_ext;
   double inv_freq[kMaxPairs];     // theta^(-2i/head_dim)
 };
 
@@ -98,7 +104,7 @@ int axis_of_pair(AxisMapId id, int i);
 // Launchers (return the hipError_t of the launch).
 hipError_t launch_reassign(const ReassignParams &p, hipStream_t stream);
 hipError_t launch_rebind(const RebindParams &p, prcr_dtype dtype, int head_dim, AxisMapId map,
-                         bool paged, hipStream_t stream);
+                         bool paged, bool fused, hipStream_t stream);
 hipError_t launch_store(const StoreParams &p, hipStream_t stream);
 
 }  // namespace prcr

@@ -8,13 +8,13 @@
 #include <climits>
 #include <cmath>
 
+#include "positions.h"
 #include "prcr_internal.h"
 
 namespace prcr {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr double kExact = 9007199254740992.0;   // 2^53
 
 __device__ __forceinline__ int wave_min(int v) {
   for (int o = kWave / 2; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
@@ -23,36 +23,6 @@ __device__ __forceinline__ int wave_min(int v) {
 __device__ __forceinline__ int wave_max(int v) {
   for (int o = kWave / 2; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
   return v;
-}
-
-// (p_txt - L) + (L + 1)(D + (K - 1)(c - lo)) / ((K + 1) D), or the interval
-// centre for a degenerate axis.  Sets *range_bad when the integer rational is
-// not exactly representable (then the value is a close double approximation).
-__device__ __forceinline__ double pcr_position(int64_t p_txt, int64_t L, int64_t K, int64_t lo,
-                                               int64_t hi, int64_t c, bool *range_bad) {
-  const int64_t A = p_txt - L;
-  int64_t span = hi - lo;
-  if (span <= 0) {
-    // u = 1/2:  A + (L + 1)/2 = (2A + L + 1) / 2
-    const double mag = 2.0 * fabs(static_cast<double>(A)) + static_cast<double>(L + 1);
-    if (mag >= kExact) {
-      *range_bad = true;
-      return static_cast<double>(A) + 0.5 * static_cast<double>(L + 1);
-    }
-    return static_cast<double>(2 * A + L + 1) / 2.0;
-  }
-  const double kd = static_cast<double>(K + 1) * static_cast<double>(span);
-  const double mag = (fabs(static_cast<double>(A)) + static_cast<double>(L + 1)) * kd;
-  if (mag >= kExact * 0.5 || kd >= kExact) {
-    *range_bad = true;
-    const double frac = static_cast<double>(L + 1) *
-                        (static_cast<double>(span) + static_cast<double>(K - 1) * static_cast<double>(c - lo)) /
-                        kd;
-    return static_cast<double>(A) + frac;
-  }
-  const int64_t den = (K + 1) * span;
-  const int64_t num = A * den + (L + 1) * (span + (K - 1) * (c - lo));
-  return static_cast<double>(num) / static_cast<double>(den);
 }
 
 __global__ __launch_bounds__(kThreads) void reassign_kernel(const ReassignParams p) {
@@ -136,51 +106,18 @@ __global__ __launch_bounds__(kThreads) void reassign_kernel(const ReassignParams
       out[0] = out[1] = out[2] = __builtin_nan("");
       continue;
     }
+    bool rb = false;
 #pragma unroll
-    for (int a = 0; a < 3; ++a) {
-      const int64_t c = coords_b[3 * m + a];
-      double v;
-      switch (p.mode) {
-        case PRCR_MODE_SHIFT:
-          v = static_cast<double>(p_txt + 1 + (c - lo[a]));
-          break;
-        case PRCR_MODE_IDENTITY:
-          v = static_cast<double>(c);
-          break;
-        case PRCR_MODE_LPA:
-          v = static_cast<double>(p_txt + j + 1);
-          break;
-        case PRCR_MODE_UIR: {
-          const double mag = fabs(static_cast<double>(p_txt)) * static_cast<double>(K + 1) + K + 1;
-          if (mag >= kExact) {
-            range_bad = 1;
-            v = static_cast<double>(p_txt) + static_cast<double>(j + 1) / static_cast<double>(K + 1);
-          } else {
-            v = static_cast<double>(p_txt * (K + 1) + j + 1) / static_cast<double>(K + 1);
-          }
-          break;
-        }
-        default: {
-          bool rb = false;
-          v = pcr_position(p_txt, L, K, lo[a], hi[a], c, &rb);
-          range_bad |= rb ? 1 : 0;
-          break;
-        }
-      }
-      out[a] = v;
-    }
+    for (int a = 0; a < 3; ++a)
+      out[a] = reassigned(p.mode, p_txt, L, K, j, lo[a], hi[a], coords_b[3 * m + a], &rb);
+    range_bad |= rb ? 1 : 0;
   }
 
   if (tid == 0) {
-    int64_t next = p_txt + 1;
-    if (p.mode == PRCR_MODE_LPA) {
-      next = p_txt + K + 1;
-    } else if (p.mode == PRCR_MODE_SHIFT && any_valid) {
-      int64_t span = 0;
-      for (int a = 0; a < 3; ++a)
-        span = max(span, static_cast<int64_t>(hi[a]) - static_cast<int64_t>(lo[a]));
-      next = p_txt + 2 + span;
-    }
+    int64_t span = 0;
+    for (int a = 0; a < 3; ++a)
+      span = max(span, static_cast<int64_t>(hi[a]) - static_cast<int64_t>(lo[a]));
+    const int64_t next = next_text_position(p.mode, p_txt, K, any_valid, span);
     p.next_pos[b] = static_cast<int32_t>(next);
     if (bad && p.err != nullptr) atomicOr(p.err, PRCR_DERR_INDEX);
   }

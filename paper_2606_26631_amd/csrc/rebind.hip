@@ -11,6 +11,7 @@
 // with 16-byte non-temporal accesses: every byte is touched exactly once.
 #include <cmath>
 
+#include "positions.h"
 #include "prcr_internal.h"
 
 namespace prcr {
@@ -83,8 +84,8 @@ struct Store<uint16_t> {
 };
 
 // Compile-time launch shape, chosen by measurement on MI355X: 4 waves per
-// workgroup, 2 row iterations in flight per wave, about 72 rows per wave, keys
-// and values in separate halves of the grid, non-temporal 16-byte accesses.
+// workgroup, 2 row iterations per batch of loads, about 72 rows per wave on large
+// problems, non-temporal 16-byte accesses.
 #ifndef PRCR_WAVES_PER_BLOCK
 #define PRCR_WAVES_PER_BLOCK 4
 #endif
@@ -93,9 +94,6 @@ struct Store<uint16_t> {
 #endif
 #ifndef PRCR_ROWS_PER_WAVE
 #define PRCR_ROWS_PER_WAVE 72
-#endif
-#ifndef PRCR_SPLIT_KV
-#define PRCR_SPLIT_KV 1
 #endif
 #ifndef PRCR_NONTEMPORAL
 #define PRCR_NONTEMPORAL 1
@@ -117,17 +115,30 @@ __device__ __forceinline__ void store16(char *p, u32x4 v) {
 }
 
 // One wavefront = one selected token x one run of rows_per_wave (layer, head)
-// rows of it.  With kSplitKV the top of the flat workgroup index picks the
-// array: the first half rotates and stores keys, the second half copies values.
-// Workgroups are dispatched in index order, so the key half runs before the
-// value half and each wave streams one source and one destination, which
-// measured faster than moving both arrays in one wave.
-template <typename T, int D, class Map, bool kPaged, int kWaves, int kUnroll, bool kSplitKV>
+// rows x one array.  The top of the flat workgroup index picks the array: the
+// first half rotates and stores keys, the second half copies values.  Workgroups
+// are dispatched in index order, so the key half runs before the value half and
+// each wave streams one source and one destination (faster than moving both
+// arrays in one wave).
+//
+// Latency: the wave issues the loads of its first rows as soon as the source row
+// is known to be in range, before the remaining validation, position and cos/sin
+// work, and afterwards always loads the next batch of rows while it stores the
+// current one.
+//
+// kFused (the single-launch revisit): instead of reading new_pos, each key wave
+// reduces its sequence's coordinate ranges over the selection (Eq. (8)) with
+// wave shuffles and computes its own token's position (Eq. (9)-(10)); the first
+// token's wave also writes the sequence's next text position.  The reduction
+// costs K_b coordinate reads per wave, which is small at the selection sizes
+// the fused path is meant for.
+template <typename T, int D, class Map, bool kPaged, int kWaves, int kUnroll, bool kFused>
 __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const RebindParams p) {
   constexpr int P = D / 2;
   constexpr int E = Store<T>::kPerChunk;   // elements per 16-byte chunk
   constexpr int LPR = P / E;               // lanes per row
   constexpr int RPI = kWave / LPR;         // rows per wave and iteration
+  constexpr int kStep = RPI * kUnroll;     // rows per batch of loads
   constexpr int kRowBytes = D * static_cast<int>(sizeof(T));
   constexpr int kHalfBytes = kRowBytes / 2;
   static_assert(Map::kPairs == P, "axis map does not match head_dim");
@@ -141,30 +152,35 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
   // take consecutive tokens, so the work in flight spreads over many sequences,
   // memory rows and cache rows at once; orders that concentrate it on fewer
   // sequences, or give each XCD its own contiguous range, measured slower.
-  constexpr int nkv = kSplitKV ? 2 : 1;
   const int64_t n_tblk = (static_cast<int64_t>(p.total_k) + kWaves - 1) / kWaves;
-  const int64_t n_work = n_tblk * p.n_row_groups * nkv;
+  const int64_t n_work = n_tblk * p.n_row_groups * 2;
   const int64_t L = blockIdx.x;
-  // New cache lengths, written once by the first workgroup (also when total_k = 0).
-  if (L == 0 && p.new_cache_len != nullptr) {
-    for (int b = threadIdx.x; b < p.batch; b += blockDim.x)
-      p.new_cache_len[b] = p.cache_len[b] + (p.sel_off[b + 1] - p.sel_off[b]);
+  // New cache lengths (and, fused, the next position of empty selections),
+  // written once by the first workgroup (also when total_k = 0).
+  if (L == 0) {
+    for (int b = threadIdx.x; b < p.batch; b += blockDim.x) {
+      const int kb = p.sel_off[b + 1] - p.sel_off[b];
+      if (p.new_cache_len != nullptr) p.new_cache_len[b] = p.cache_len[b] + kb;
+      if (kFused && kb == 0)
+        p.next_pos[b] = static_cast<int32_t>(next_text_position(p.mode, p.p_txt[b], 0, false, 0));
+    }
   }
   if (L >= n_work) return;
   const int64_t tblk = L % n_tblk;
   const int grp = static_cast<int>((L / n_tblk) % p.n_row_groups);
-  const int kv = static_cast<int>(L / (n_tblk * p.n_row_groups));
-  const bool keys = !kSplitKV || kv == 0;
-  const bool values = !kSplitKV || kv == 1;
+  const bool keys = L < n_tblk * p.n_row_groups;
   const int g = static_cast<int>(tblk * kWaves + wave);
   if (g >= p.total_k) return;
   const int r = lane / LPR;   // this lane's row within an iteration
   const int c = lane % LPR;   // this lane's 16-byte chunk of a half row
+  const int rows_total = p.n_layers * p.n_kv_heads;
+  const int row0 = grp * p.rows_per_wave;
+  const int row_end = min(rows_total, row0 + p.rows_per_wave);
 
   // Loads that depend only on g are issued first ...
   const int m = p.sel_idx[g];
   double pt = 0.0, ph = 0.0, pw = 0.0;
-  if (keys) {
+  if (!kFused && keys) {
     pt = p.new_pos[3 * static_cast<int64_t>(g) + 0];
     ph = p.new_pos[3 * static_cast<int64_t>(g) + 1];
     pw = p.new_pos[3 * static_cast<int64_t>(g) + 2];
@@ -178,7 +194,23 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
     cnt += __popcll(__ballot(le));
   }
   const int b = __builtin_amdgcn_readfirstlane(cnt - 1);
-  // ... and the per-sequence values, all at once from a clamped index.
+
+  // The source rows exist whenever b and m are in range: start loading them.
+  const bool src_ok = b >= 0 && b < p.batch && m >= 0 && m < p.max_visual;
+  const size_t tok_off = src_ok ? (static_cast<size_t>(b) * p.max_visual + m) * rows_total : 0;
+  const char *src = static_cast<const char *>(keys ? p.mem_k : p.mem_v) + tok_off * kRowBytes + c * 16;
+  char *dst = static_cast<char *>(keys ? p.cache_k : p.cache_v) + c * 16;
+  u32x4 lo[kUnroll], hi[kUnroll];
+#pragma unroll
+  for (int u = 0; u < kUnroll; ++u) {
+    const int row = row0 + u * RPI + r;
+    if (src_ok && row < row_end) {
+      lo[u] = load16(src + static_cast<size_t>(row) * kRowBytes);
+      hi[u] = load16(src + static_cast<size_t>(row) * kRowBytes + kHalfBytes);
+    }
+  }
+
+  // Per-sequence values, all at once from a clamped index, and validation.
   const int bq = min(max(b, 0), p.batch - 1);
   const int s0 = p.sel_off[bq];
   const int s1 = p.sel_off[bq + 1];
@@ -186,12 +218,63 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
   const int64_t slot = static_cast<int64_t>(p.cache_len[bq]) + (g - s0);
 
   int flags = 0;
-  bool ok = b >= 0 && b < p.batch && s0 <= g && g < s1;
+  const bool offsets_ok = b >= 0 && b < p.batch && s0 <= g && g < s1;
+  bool ok = offsets_ok;
   if (!ok) {
     flags = PRCR_DERR_OFFSETS;
   } else if (m < 0 || m >= nvis || m >= p.max_visual) {
     ok = false;
     flags = PRCR_DERR_INDEX;
+  }
+  if constexpr (kFused) {
+    if (keys && offsets_ok) {
+      // Eq. (8): ranges of the sequence's valid selected coordinates.
+      const int K = s1 - s0;
+      const int lim = min(nvis, p.max_visual);
+      const int32_t *cb = p.coords + static_cast<int64_t>(b) * p.max_visual * 3;
+      int lo0 = INT_MAX, lo1 = INT_MAX, lo2 = INT_MAX, hi0 = INT_MIN, hi1 = INT_MIN, hi2 = INT_MIN;
+      for (int j = lane; j < K; j += kWave) {
+        const int mj = p.sel_idx[s0 + j];
+        if (mj >= 0 && mj < lim) {
+          const int c0 = cb[3 * mj], c1 = cb[3 * mj + 1], c2 = cb[3 * mj + 2];
+          lo0 = min(lo0, c0); hi0 = max(hi0, c0);
+          lo1 = min(lo1, c1); hi1 = max(hi1, c1);
+          lo2 = min(lo2, c2); hi2 = max(hi2, c2);
+        }
+      }
+      for (int o = kWave / 2; o > 0; o >>= 1) {
+        lo0 = min(lo0, __shfl_xor(lo0, o)); hi0 = max(hi0, __shfl_xor(hi0, o));
+        lo1 = min(lo1, __shfl_xor(lo1, o)); hi1 = max(hi1, __shfl_xor(hi1, o));
+        lo2 = min(lo2, __shfl_xor(lo2, o)); hi2 = max(hi2, __shfl_xor(hi2, o));
+      }
+      const int64_t ptxt = p.p_txt[b];
+      bool range_bad = false;
+      if (ok) {
+        const int32_t *cm = cb + 3 * static_cast<int64_t>(m);
+        const int64_t j = g - s0;
+        pt = reassigned(p.mode, ptxt, p.l_ext, K, j, lo0, hi0, cm[0], &range_bad);
+        ph = reassigned(p.mode, ptxt, p.l_ext, K, j, lo1, hi1, cm[1], &range_bad);
+        pw = reassigned(p.mode, ptxt, p.l_ext, K, j, lo2, hi2, cm[2], &range_bad);
+      } else {
+        pt = ph = pw = __builtin_nan("");
+      }
+      if (grp == 0 && lane == 0) {
+        if (p.pos_out != nullptr) {
+          p.pos_out[3 * static_cast<int64_t>(g) + 0] = pt;
+          p.pos_out[3 * static_cast<int64_t>(g) + 1] = ph;
+          p.pos_out[3 * static_cast<int64_t>(g) + 2] = pw;
+        }
+        if (g == s0) {
+          const bool any_valid = lo0 <= hi0;
+          const int64_t span = any_valid ? max(static_cast<int64_t>(hi0) - lo0,
+                                               max(static_cast<int64_t>(hi1) - lo1,
+                                                   static_cast<int64_t>(hi2) - lo2))
+                                         : 0;
+          p.next_pos[b] = static_cast<int32_t>(next_text_position(p.mode, ptxt, K, any_valid, span));
+        }
+        if (range_bad && p.err != nullptr) atomicOr(p.err, PRCR_DERR_RANGE);
+      }
+    }
   }
   int64_t slot_id = -1, blk = 0, off = 0;
   if (ok) {
@@ -223,10 +306,6 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
   }
   if (!ok) return;
 
-  const int rows_total = p.n_layers * p.n_kv_heads;
-  const int row0 = grp * p.rows_per_wave;
-  const int row_end = min(rows_total, row0 + p.rows_per_wave);
-  const size_t tok_off = (static_cast<size_t>(b) * p.max_visual + m) * rows_total;
   // Destination row offsets (in rows of head_dim elements).
   size_t dst_base;
   if constexpr (kPaged) {
@@ -245,114 +324,117 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
     }
   };
 
+  // cos/sin of this token's angles (keys only): lane i computes pair i (mod P),
+  // then lane (r, c) gathers the pairs c*E .. c*E+E-1 of its two chunks.
+  double cs[E], sn[E];
   if (keys) {
-    // cos/sin of this token's angles: lane i computes pair i (mod P), then lane
-    // (r, c) gathers the pairs c*E .. c*E+E-1 of its two chunks by shuffles.
     const int pair = lane % P;
     const int ax = Map::axis(pair);
     double sv, cv;
     sincos((ax == 0 ? pt : (ax == 1 ? ph : pw)) * p.inv_freq[pair], &sv, &cv);
-    double cs[E], sn[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       cs[e] = __shfl(cv, c * E + e);
       sn[e] = __shfl(sv, c * E + e);
     }
-    const char *src = static_cast<const char *>(p.mem_k) + tok_off * kRowBytes + c * 16;
-    char *dst = static_cast<char *>(p.cache_k) + c * 16;
-    for (int rb = row0; rb < row_end; rb += RPI * kUnroll) {
-      u32x4 lo[kUnroll], hi[kUnroll];
+  }
+
+  for (int rb = row0; rb < row_end; rb += kStep) {
+    // next batch in flight while this one is stored
+    u32x4 nlo[kUnroll], nhi[kUnroll];
+    const int nb = rb + kStep;
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int row = rb + u * RPI + r;
-        if (row < row_end) {
-          lo[u] = load16(src + static_cast<size_t>(row) * kRowBytes);
-          hi[u] = load16(src + static_cast<size_t>(row) * kRowBytes + kHalfBytes);
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int row = rb + u * RPI + r;
-        if (row < row_end) {
-          u32x4 ol, oh;
-          Store<T>::rotate(lo[u], hi[u], cs, sn, ol, oh);
-          const size_t d = dst_offset(row);
-          store16(dst + d, ol);
-          store16(dst + d + kHalfBytes, oh);
-        }
+    for (int u = 0; u < kUnroll; ++u) {
+      const int row = nb + u * RPI + r;
+      if (row < row_end) {
+        nlo[u] = load16(src + static_cast<size_t>(row) * kRowBytes);
+        nhi[u] = load16(src + static_cast<size_t>(row) * kRowBytes + kHalfBytes);
       }
     }
-  }
-  if (values) {
-    const char *src = static_cast<const char *>(p.mem_v) + tok_off * kRowBytes + c * 16;
-    char *dst = static_cast<char *>(p.cache_v) + c * 16;
-    for (int rb = row0; rb < row_end; rb += RPI * kUnroll) {
-      u32x4 lo[kUnroll], hi[kUnroll];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int row = rb + u * RPI + r;
-        if (row < row_end) {
-          lo[u] = load16(src + static_cast<size_t>(row) * kRowBytes);
-          hi[u] = load16(src + static_cast<size_t>(row) * kRowBytes + kHalfBytes);
-        }
+    for (int u = 0; u < kUnroll; ++u) {
+      const int row = rb + u * RPI + r;
+      if (row < row_end) {
+        u32x4 ol = lo[u], oh = hi[u];
+        if (keys) Store<T>::rotate(lo[u], hi[u], cs, sn, ol, oh);
+        const size_t d = dst_offset(row);
+        store16(dst + d, ol);
+        store16(dst + d + kHalfBytes, oh);
       }
+    }
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int row = rb + u * RPI + r;
-        if (row < row_end) {
-          const size_t d = dst_offset(row);
-          store16(dst + d, lo[u]);
-          store16(dst + d + kHalfBytes, hi[u]);
-        }
-      }
+    for (int u = 0; u < kUnroll; ++u) {
+      lo[u] = nlo[u];
+      hi[u] = nhi[u];
     }
   }
 }
 
 constexpr int kWavesPerBlock = PRCR_WAVES_PER_BLOCK;
 constexpr int kUnrollRows = PRCR_UNROLL;
-constexpr bool kSplit = PRCR_SPLIT_KV != 0;
 
-template <typename T, int D, class Map, bool kPaged>
+template <typename T, int D, class Map, bool kPaged, bool kFused>
 hipError_t launch_one(const RebindParams &in, hipStream_t stream) {
   constexpr int P = D / 2;
   constexpr int LPR = P / Store<T>::kPerChunk;
   constexpr int RPI = kWave / LPR;
+  constexpr int kStep = RPI * kUnrollRows;
   RebindParams p = in;
-  // Rows of one token handled by one wave: a whole number of iterations, about
-  // PRCR_ROWS_PER_WAVE, spread evenly over the token's n_layers * n_kv_heads rows.
+  // Rows of one token handled by one wave: a whole number of load batches.
+  // Large problems use about PRCR_ROWS_PER_WAVE rows per wave; small ones are
+  // spread over at least kMinWaves waves per array (down to one batch per wave)
+  // so that their latency is a few load round trips.
+  constexpr int64_t kMinWaves = 4096;
   const int rows_total = p.n_layers * p.n_kv_heads;
-  const int step = RPI * kUnrollRows;
-  const int target = (PRCR_ROWS_PER_WAVE + step - 1) / step * step;
-  const int groups = (rows_total + target - 1) / target;
-  int per = (rows_total + groups - 1) / groups;
-  per = (per + step - 1) / step * step;
-  p.rows_per_wave = per;
-  p.n_row_groups = (rows_total + per - 1) / per;
+  const int64_t rows_all = static_cast<int64_t>(p.total_k) * rows_total;
+  int64_t target = PRCR_ROWS_PER_WAVE;
+  if (rows_all < target * kMinWaves) target = rows_all / kMinWaves;
+  target = (target + kStep - 1) / kStep * kStep;
+  if (target < kStep) target = kStep;
+  const int64_t groups = (rows_total + target - 1) / target;
+  int64_t per = (rows_total + groups - 1) / groups;
+  per = (per + kStep - 1) / kStep * kStep;
+  p.rows_per_wave = static_cast<int32_t>(per);
+  p.n_row_groups = static_cast<int32_t>((rows_total + per - 1) / per);
   if (p.n_row_groups > 65535) return hipErrorInvalidConfiguration;
   // One flat grid over (token block, row group, K|V); at least one workgroup so
   // that the new cache lengths are written when nothing is selected.
   const int64_t n_tblk = (static_cast<int64_t>(p.total_k) + kWavesPerBlock - 1) / kWavesPerBlock;
-  int64_t n_work = n_tblk * p.n_row_groups * (kSplit ? 2 : 1);
+  int64_t n_work = n_tblk * p.n_row_groups * 2;
   if (n_work < 1) n_work = 1;
   if (n_work > INT32_MAX) return hipErrorInvalidConfiguration;
   const dim3 grid(static_cast<unsigned>(n_work));
-  rebind_inject_kernel<T, D, Map, kPaged, kWavesPerBlock, kUnrollRows, kSplit>
+  rebind_inject_kernel<T, D, Map, kPaged, kWavesPerBlock, kUnrollRows, kFused>
       <<<grid, kWavesPerBlock * kWave, 0, stream>>>(p);
   return hipGetLastError();
 }
 
-template <typename T, bool kPaged>
+template <typename T, bool kPaged, bool kFused>
 hipError_t dispatch_map(const RebindParams &p, int head_dim, AxisMapId map, hipStream_t stream) {
   if (head_dim == 64) {
-    if (map == AxisMapId::kS_8_12_12) return launch_one<T, 64, Sectioned<8, 12, 12>, kPaged>(p, stream);
-    if (map == AxisMapId::kI_11_11_10) return launch_one<T, 64, Interleaved<11, 11, 10>, kPaged>(p, stream);
+    if (map == AxisMapId::kS_8_12_12)
+      return launch_one<T, 64, Sectioned<8, 12, 12>, kPaged, kFused>(p, stream);
+    if (map == AxisMapId::kI_11_11_10)
+      return launch_one<T, 64, Interleaved<11, 11, 10>, kPaged, kFused>(p, stream);
   } else if (head_dim == 128) {
-    if (map == AxisMapId::kS_16_24_24) return launch_one<T, 128, Sectioned<16, 24, 24>, kPaged>(p, stream);
-    if (map == AxisMapId::kI_22_21_21) return launch_one<T, 128, Interleaved<22, 21, 21>, kPaged>(p, stream);
-    if (map == AxisMapId::kI_24_20_20) return launch_one<T, 128, Interleaved<24, 20, 20>, kPaged>(p, stream);
+    if (map == AxisMapId::kS_16_24_24)
+      return launch_one<T, 128, Sectioned<16, 24, 24>, kPaged, kFused>(p, stream);
+    if (map == AxisMapId::kI_22_21_21)
+      return launch_one<T, 128, Interleaved<22, 21, 21>, kPaged, kFused>(p, stream);
+    if (map == AxisMapId::kI_24_20_20)
+      return launch_one<T, 128, Interleaved<24, 20, 20>, kPaged, kFused>(p, stream);
   }
   return hipErrorInvalidValue;
+}
+
+template <typename T>
+hipError_t dispatch_layout(const RebindParams &p, int head_dim, AxisMapId map, bool paged,
+                           bool fused, hipStream_t stream) {
+  if (paged)
+    return fused ? dispatch_map<T, true, true>(p, head_dim, map, stream)
+                 : dispatch_map<T, true, false>(p, head_dim, map, stream);
+  return fused ? dispatch_map<T, false, true>(p, head_dim, map, stream)
+               : dispatch_map<T, false, false>(p, head_dim, map, stream);
 }
 
 }  // namespace
@@ -382,12 +464,9 @@ int axis_of_pair(AxisMapId id, int i) {
 }
 
 hipError_t launch_rebind(const RebindParams &p, prcr_dtype dtype, int head_dim, AxisMapId map,
-                         bool paged, hipStream_t stream) {
-  if (dtype == PRCR_F32)
-    return paged ? dispatch_map<float, true>(p, head_dim, map, stream)
-                 : dispatch_map<float, false>(p, head_dim, map, stream);
-  return paged ? dispatch_map<uint16_t, true>(p, head_dim, map, stream)
-               : dispatch_map<uint16_t, false>(p, head_dim, map, stream);
+                         bool paged, bool fused, hipStream_t stream) {
+  if (dtype == PRCR_F32) return dispatch_layout<float>(p, head_dim, map, paged, fused, stream);
+  return dispatch_layout<uint16_t>(p, head_dim, map, paged, fused, stream);
 }
 
 }  // namespace prcr

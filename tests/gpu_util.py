@@ -77,17 +77,22 @@ class Case:
 
 
 def run_both(case: Case, sel_off, sel_idx, p_txt, cache_len, mode="pcr", l_ext=2,
-             stream=None):
-    """Reassign + rebind/inject on the GPU and in the oracle; returns (gpu, ref) dicts."""
+             stream=None, fused=False):
+    """Reassign + rebind/inject on the GPU (two calls, or the single fused
+    prcr_revisit launch) and in the oracle; returns (gpu, ref) dicts."""
     w = case.w
     mem, cache = case.memory(), case.cache()
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
     so, si = to_dev(np.asarray(sel_off, np.int32)), to_dev(np.asarray(sel_idx, np.int32))
-    new_pos, next_pos = prcr.reassign_coords(mem, so, si, to_dev(np.asarray(p_txt, np.int32)),
-                                             mode, l_ext, err=err, stream=stream)
-    new_len, slots = prcr.rebind_inject(case.rope(), mem, so, si, new_pos, cache,
-                                        to_dev(np.asarray(cache_len, np.int32)), err=err,
-                                        stream=stream)
+    pt, cl = to_dev(np.asarray(p_txt, np.int32)), to_dev(np.asarray(cache_len, np.int32))
+    if fused:
+        new_pos, next_pos, new_len, slots = prcr.revisit(case.rope(), mem, so, si, pt, cache, cl,
+                                                         mode, l_ext, err=err, stream=stream)
+    else:
+        new_pos, next_pos = prcr.reassign_coords(mem, so, si, pt, mode, l_ext, err=err,
+                                                 stream=stream)
+        new_len, slots = prcr.rebind_inject(case.rope(), mem, so, si, new_pos, cache, cl, err=err,
+                                            stream=stream)
     torch.cuda.synchronize()
     gpu = {"new_pos": new_pos.cpu().numpy(), "next_pos": next_pos.cpu().numpy(),
            "slot_mapping": slots.cpu().numpy(), "new_cache_len": new_len.cpu().numpy(),

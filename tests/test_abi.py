@@ -150,3 +150,26 @@ def test_store_validation_errors():
     assert call_store(mem, s_src=0) == 2
     assert call_store(mem, raw_k=None) == 1
     assert call_store(mem, raw_k=FAKE + 8) == 4
+
+
+def call_revisit(rope, mem, cache, mode=0, l_ext=2, p_txt=FAKE, next_pos=FAKE + 0x200,
+                 new_pos=None, cache_len=FAKE, new_len=FAKE + 0x100):
+    L = prcr.lib()
+    return L.prcr_revisit(ctypes.byref(rope), ctypes.byref(mem) if mem is not None else None,
+                          FAKE, FAKE, 10, p_txt, mode, l_ext, ctypes.byref(cache), cache_len,
+                          new_pos, next_pos, new_len, FAKE, None, None)
+
+
+def test_revisit_validation_errors():
+    rope, mem, cache = good()
+    assert call_revisit(rope, None, cache) == 1
+    assert call_revisit(rope, mem, cache, p_txt=None) == 1
+    assert call_revisit(rope, mem, cache, next_pos=None) == 1
+    assert call_revisit(rope, mem, cache, mode=7) == 5
+    assert call_revisit(rope, mem, cache, l_ext=-2) == 5
+    assert call_revisit(rope, mem, cache, new_pos=FAKE + 4) == 4
+    assert call_revisit(rope, mem, cache, new_len=FAKE) == 7
+    r2, m2, c2 = good(); m2.coords = None
+    assert call_revisit(r2, m2, c2) == 1
+    r2, m2, c2 = good(); r2.section[0], r2.section[1] = 32, 8
+    assert call_revisit(r2, m2, c2) == 6

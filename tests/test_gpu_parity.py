@@ -209,3 +209,108 @@ def test_store_raw(dtype):
     assert int(err.item()) == e_all == oracle.ERR_INDEX
     assert np.array_equal(workloads.as_numpy_storage(mem.k), ek)
     assert np.array_equal(workloads.as_numpy_storage(mem.v), ev)
+
+
+# ---------------------------------------------------------------------------
+# The fused single-launch revisit (prcr_revisit) against the same oracle.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("cfg", [1, 2, 3, 5])
+def test_fused_workload_small(cfg):
+    w = workloads.make(cfg, "small")
+    _say(f"fused: workload {cfg} small")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len, fused=True)
+    assert_parity(case, gpu, ref)
+
+
+@pytest.mark.parametrize("mode", ["pcr", "shift", "identity", "lpa", "uir"])
+def test_fused_modes(mode):
+    w = workloads.make(3, "small")
+    _say(f"fused: workload 3 small, mode {mode}")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len, mode=mode, l_ext=3,
+                        fused=True)
+    assert_parity(case, gpu, ref)
+
+
+@pytest.mark.parametrize("paged", [False, True])
+@pytest.mark.parametrize("dtype,D,sections,inter", [COMPILED[0], COMPILED[4], COMPILED[7],
+                                                    COMPILED[9]])
+def test_fused_ragged_edges(dtype, D, sections, inter, paged):
+    w = workloads.custom(B=5, NL=3, H=3, D=D, dtype=dtype, sections=sections, interleaved=inter,
+                         theta=5e6 if inter else 1e6, frames=2, gh=9, gw=7,
+                         ks=(0, 1, 13, 0, 30), lens=(0, 11, 29, 3, 40), paged=paged, block_size=7)
+    _say(f"fused: custom {dtype} D={D} {sections} inter={inter} paged={paged}")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len, mode="shift", fused=True)
+    assert_parity(case, gpu, ref)
+
+
+def test_fused_data_errors():
+    w = workloads.custom(B=3, NL=2, H=2, ks=(6, 4, 5), lens=(10, 25, 5), s_max=28)
+    sel_idx = w.sel_idx.copy()
+    sel_idx[0] = w.M_max + 3          # the first token of sequence 0 is invalid
+    sel_idx[3] = -1
+    _say("fused: bad indices (including a sequence's first token) + capacity overflow")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, sel_idx, w.p_txt, w.cache_len, fused=True)
+    assert ref["err"] == (oracle.ERR_INDEX | oracle.ERR_CAPACITY)
+    assert_parity(case, gpu, ref)
+
+
+def test_fused_video_four_revisits():
+    w = workloads.make(4, "small")
+    _say("fused: workload 4 small, 4 revisits")
+    case = Case(w)
+    lens = w.cache_len.astype(np.int64).copy()
+    p_txt = w.p_txt.astype(np.int64).copy()
+    for so, si in w.revisits:
+        gpu, ref = run_both(case, so, si, p_txt, lens, fused=True)
+        assert_parity(case, gpu, ref)
+        lens = ref["new_cache_len"] + w.decode_between
+        p_txt = ref["next_pos"] + w.decode_between - 1
+
+
+def test_graph_replays_match_eager():
+    """prcr_revisit captured in a HIP graph: every replay, with eager work that
+    clobbers the target rows in between, reproduces the eager result."""
+    w = workloads.make(5, "small")
+    _say("graph capture of prcr_revisit (workload 5 small), 3 replays")
+    case = Case(w)
+    mem, cache, rope = case.memory(), case.cache(), case.rope()
+    so, si = to_dev(w.sel_off), to_dev(w.sel_idx)
+    pt, cl = to_dev(w.p_txt), to_dev(w.cache_len)
+    new_pos = torch.empty((w.total_k, 3), dtype=torch.float64, device=DEV)
+    next_pos = torch.empty((w.B,), dtype=torch.int32, device=DEV)
+    new_len = torch.empty((w.B,), dtype=torch.int32, device=DEV)
+    slots = torch.empty((w.total_k,), dtype=torch.int64, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    s = torch.cuda.Stream(device=DEV)
+    torch.cuda.synchronize()
+
+    def call():
+        prcr.revisit(rope, mem, so, si, pt, cache, cl, "pcr", 2, new_pos, next_pos, new_len,
+                     slots, err, s)
+
+    with torch.cuda.stream(s):
+        call()
+    torch.cuda.synchronize()
+    eager = [t.clone() for t in (cache.k, cache.v, new_pos, next_pos, new_len, slots)]
+    blk = slots // w.block_size
+    off = slots % w.block_size
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        call()
+    torch.cuda.synchronize()
+    for r in range(3):
+        cache.k[:, blk, off] = 0                    # eager work between replays
+        cache.v[:, blk, off] = 0
+        new_pos.zero_(); next_pos.zero_(); new_len.zero_(); slots.fill_(-7)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip((cache.k, cache.v, new_pos, next_pos, new_len, slots), eager):
+            assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a,
+                               b.view(torch.int16) if b.dtype == torch.bfloat16 else b), f"replay {r}"
+    assert int(err.item()) == 0

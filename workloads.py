@@ -307,3 +307,27 @@ def custom(B=3, NL=2, H=2, D=128, dtype="bf16", sections=(16, 24, 24), interleav
     return Workload(0, "custom", dtype, B, NL, H, D, M, tuple(sections), bool(interleaved),
                     float(theta), coords, np.full(B, M, np.int32), off, idx,
                     (lens - 1).astype(np.int32), lens, **kw)
+
+
+PAPER_MODELS = {
+    # Table 3's operating points: decoder shape of the paper's Qwen3-VL models
+    # (public configurations: 36 / 64 layers, 8 KV heads, head_dim 128, interleaved
+    # M-RoPE [24, 20, 20], theta 5e6); 768 visual tokens per image (24 x 32 grid).
+    "qwen3-vl-8b": dict(NL=36, H=8),
+    "qwen3-vl-32b": dict(NL=64, H=8),
+}
+
+
+def paper_k(model: str, K: int, seed: int = 2000) -> Workload:
+    """One sequence revisiting K of 768 visual tokens at a paper model's cache shape."""
+    rng = np.random.Generator(np.random.PCG64(seed + K))
+    shape = PAPER_MODELS[model]
+    gh, gw = 24, 32
+    M = gh * gw
+    coords = _grid_coords(1, gh, gw)[None]
+    off, idx = _csr([np.sort(rng.choice(M, size=K, replace=False))])
+    lens = np.array([1024], np.int32)
+    return Workload(6, f"{model}-K{K}", "bf16", 1, shape["NL"], shape["H"], 128, M, (24, 20, 20),
+                    True, 5e6, coords, np.array([M], np.int32), off, idx,
+                    (lens - 1).astype(np.int32), lens, s_max=1024 + K, revisits=[(off, idx)],
+                    seed=seed + K)
