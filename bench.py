@@ -227,6 +227,66 @@ def small_k_latency(dev, reps=200):
     return out
 
 
+def prefill_capture_bw(dev, steps=20):
+    """Bandwidth of the fused prefill capture (one layer per call) at the 32-sequence
+    shape: 32 prompts of 256 text + 64x32 visual + 256 text tokens, 36 layers x 8 KV
+    heads, d 128, bf16, interleaved M-RoPE.  Algorithmic bytes per call: read raw K+V
+    of every prompt row, write K+V into the cache, and K+V into the memory for the
+    visual rows (2 * d * 2 bytes each)."""
+    import numpy as np
+    import torch
+
+    import paper_2606_26631_amd as prcr
+    import workloads
+    B, NL, H, D = 32, 36, 8, 128
+    pos, vis, n_tok, n_vis = workloads.prompt(B, n_before=(256,) * B, grid=((64, 32),) * B,
+                                              n_after=(256,) * B, frames=(1,) * B)
+    S = pos.shape[1]
+    M = int(n_vis.max())
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(3000)
+    raw_k = torch.randn((B, S, H, D), generator=g, device=dev).to(torch.bfloat16)
+    raw_v = torch.randn((B, S, H, D), generator=g, device=dev).to(torch.bfloat16)
+    mem = prcr.Memory(torch.empty((B, M, NL, H, D), dtype=torch.bfloat16, device=dev),
+                      torch.empty((B, M, NL, H, D), dtype=torch.bfloat16, device=dev),
+                      torch.zeros((B, M, 3), dtype=torch.int32, device=dev), t(n_vis))
+    s_max = S + 256
+    cache = prcr.Cache(torch.empty((B, NL, H, s_max, D), dtype=torch.bfloat16, device=dev),
+                       torch.empty((B, NL, H, s_max, D), dtype=torch.bfloat16, device=dev))
+    rope = prcr.Rope(D, (22, 21, 21), True, 5e6)
+    args = (t(pos), t(n_tok), t(vis))
+    start = torch.zeros(B, dtype=torch.int32, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    s = torch.cuda.Stream(device=dev)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        for layer in range(3):
+            prcr.prefill_capture(rope, mem, layer, raw_k, raw_v, *args, cache, start, True, err, s)
+        evs = []
+        for i in range(steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(s)
+            prcr.prefill_capture(rope, mem, i % NL, raw_k, raw_v, *args, cache, start, True, err, s)
+            b.record(s)
+            evs.append((a, b))
+        torch.cuda.synchronize()
+    if int(err.item()) != 0:
+        raise RuntimeError("device reported a data error in the prefill capture runs")
+    ms = [a.elapsed_time(b) for a, b in evs]
+    mean_s = sum(ms) / len(ms) / 1e3
+    rows = int(n_tok.sum()) * H
+    vrows = int(n_vis.sum()) * H
+    nbytes = (rows * 2 * 2 + vrows * 2) * D * 2
+    del mem, cache, raw_k, raw_v
+    torch.cuda.empty_cache()
+    return {"kernel": "prcr_prefill_capture", "workload": f"{B} prompts x {S} tokens "
+            f"({int(n_vis[0])} visual), {NL} layers x {H} KV heads, d {D}, bf16, one layer per call",
+            "mean_launch_us": round(mean_s * 1e6, 2), "algorithmic_bytes_per_call": nbytes,
+            "achieved": round(nbytes / mean_s / 1e9, 1), "unit": "GB/s",
+            "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4)}
+
+
 def roofline(w, rebind_ms, traffic):
     mean_s = sum(rebind_ms) / len(rebind_ms) / 1e3
     gbs = w.algorithmic_bytes() / mean_s / 1e9
@@ -302,6 +362,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-small-k", action="store_true", help="skip the small-K latency section")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-capture section")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the rebinding path shards by sequence, KV head or "
@@ -341,6 +402,8 @@ def main():
             out["secondary"]["roofline"]["achieved"] / copy["achieved"], 4)
     if not args.no_small_k:
         out["small_k_latency"] = small_k_latency(dev)
+    if not args.no_prefill:
+        out["prefill_capture"] = prefill_capture_bw(dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, dev, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -197,6 +197,34 @@ prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem,
                                int32_t *err_flag, hipStream_t stream);
 
 /*
+ * prcr_prefill_capture - one layer of the prompt prefill, fused: reads each
+ * prompt token's pre-rotary K/V rows once, writes the rotated key and the value
+ * into the standard decoder cache at the token's position ids (Eq. (4)), and
+ * writes the raw rows of visual tokens into the memory (Sec. 3.1, Eq. (6)-(7)).
+ *
+ *   raw_k, raw_v  [batch][s_src][n_kv_heads][head_dim], this layer's projections
+ *   pos           int32 [batch][s_src][3]: (t, h, w) position ids of each row
+ *   n_tokens      int32 [batch]: rows s < n_tokens[b] are prompt tokens
+ *   vis_index     int32 [batch][s_src]: visual token index m of row s, -1 if the
+ *                 row is not visual
+ *   write_coords  nonzero: also set mem->coords[b][m] = pos[b][s] (their
+ *                 original coordinates, used by IDENTITY and as p_m by PCR)
+ *   cache_start   int32 [batch]: row s goes to cache slot cache_start[b] + s
+ *                 of layer `layer`
+ * Keys are rotated as in prcr_rebind_inject (double precision, one rounding),
+ * so rebinding a visual token at its original coordinates reproduces the key
+ * written here bit for bit.  A slot beyond capacity or a bad block skips the
+ * cache row (PRCR_DERR_CAPACITY / _BLOCK); m outside [0, n_visual[b]) or
+ * n_tokens[b] outside [0, s_src] raise PRCR_DERR_INDEX.
+ */
+prcr_status prcr_prefill_capture(const prcr_rope *rope, const prcr_mem *mem, int32_t layer,
+                                 const void *raw_k, const void *raw_v, int32_t s_src,
+                                 const int32_t *pos, const int32_t *n_tokens,
+                                 const int32_t *vis_index, int32_t write_coords,
+                                 const prcr_cache *cache, const int32_t *cache_start,
+                                 int32_t *err_flag, hipStream_t stream);
+
+/*
  * prcr_revisit - the whole revisit in one launch: reassignment (Eq. (8)-(10),
  * as prcr_reassign_coords) fused with gather, rebinding and injection
  * (Eq. (11)-(13), as prcr_rebind_inject), for callers that revisit a small

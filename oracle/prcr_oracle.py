@@ -8,6 +8,9 @@ never calls it and shares no code with it.
 What it computes (Position Rebinding Cache Reuse, Sec. 3 and Algorithm 1):
 
 * ``store_raw``        - Raw Visual Evidence Memory capture, Eq. (6)-(7).
+* ``prefill_capture``  - one prefill layer: rotated keys and values into the
+                         standard cache (Eq. (4)) and raw visual rows into the
+                         memory (Eq. (6)-(7)).
 * ``reassign``         - Position-Consistent Reinsertion, Eq. (8)-(10), plus the
                          other reinsertion rules named in Sec. 3.2 / Table 2.
 * ``rotate_keys``      - RoPE rebinding of the raw keys at the new coordinates,
@@ -282,6 +285,55 @@ def store_raw(mem_k, mem_v, layer, raw_k, raw_v, vis_rows, n_visual):
             mem_k[b, m, layer] = raw_k[b, r]
             mem_v[b, m, layer] = raw_v[b, r]
     return mem_k, mem_v, err
+
+
+# --------------------------------------------------------------------------
+# Prefill capture fused with rotary: Eq. (4) and Eq. (6)-(7) for one layer
+# --------------------------------------------------------------------------
+def prefill_capture(rope: dict, mem: dict, layer: int, raw_k, raw_v, pos, n_tokens, vis_index,
+                    write_coords: bool, cache: dict, cache_start):
+    """One prefill layer: the standard cache gets RoPE(k_raw, p) and v_raw at slot
+    cache_start[b] + s (Eq. (4)); visual rows (vis_index[b][s] = m >= 0) also go raw
+    into the memory at [b][m][layer] (Eq. (6)-(7)), with their coordinates when
+    write_coords.  Returns updated copies {mem_k, mem_v, coords, k, v, err}."""
+    dtype = mem["dtype"]
+    D = rope["head_dim"]
+    invf = inv_freq(rope["theta"], D)
+    axis = pair_axis(D, rope["sections"], rope["interleaved"])
+    mk, mv = np.array(mem["k"], copy=True), np.array(mem["v"], copy=True)
+    co = np.array(mem["coords"], copy=True)
+    ck, cv = np.array(cache["k"], copy=True), np.array(cache["v"], copy=True)
+    B, S = raw_k.shape[0], raw_k.shape[1]
+    M = mk.shape[1]
+    err = 0
+    for b in range(B):
+        nt = int(n_tokens[b])
+        if nt < 0 or nt > S:
+            err |= ERR_INDEX
+        for s in range(max(0, min(nt, S))):
+            p = np.asarray(pos[b, s], dtype=np.float64)
+            y = f64_to_storage(rotate_keys(storage_to_f64(raw_k[b, s], dtype), p, invf, axis), dtype)
+            slot, where = slot_of(cache, b, int(cache_start[b]) + s)
+            if slot is None:
+                err |= where
+            elif cache["paged"]:
+                blk, off = where
+                ck[layer, blk, off] = y
+                cv[layer, blk, off] = raw_v[b, s]
+            else:
+                bb, ss = where
+                ck[bb, layer, :, ss] = y
+                cv[bb, layer, :, ss] = raw_v[b, s]
+            m = int(vis_index[b, s])
+            if m >= 0:
+                if m >= int(mem["n_visual"][b]) or m >= M:
+                    err |= ERR_INDEX
+                    continue
+                mk[b, m, layer] = raw_k[b, s]
+                mv[b, m, layer] = raw_v[b, s]
+                if write_coords:
+                    co[b, m] = pos[b, s]
+    return {"mem_k": mk, "mem_v": mv, "coords": co, "k": ck, "v": cv, "err": err}
 
 
 # --------------------------------------------------------------------------

@@ -75,6 +75,10 @@ def lib() -> ctypes.CDLL:
     L.prcr_rebind_inject.argtypes = [POINTER(CRope), POINTER(CMem), c_void_p, c_void_p, c_int32,
                                      c_void_p, POINTER(CCache), c_void_p, c_void_p, c_void_p,
                                      c_void_p, c_void_p]
+    L.prcr_prefill_capture.restype = c_int
+    L.prcr_prefill_capture.argtypes = [POINTER(CRope), POINTER(CMem), c_int32, c_void_p, c_void_p,
+                                       c_int32, c_void_p, c_void_p, c_void_p, c_int32,
+                                       POINTER(CCache), c_void_p, c_void_p, c_void_p]
     L.prcr_revisit.restype = c_int
     L.prcr_revisit.argtypes = [POINTER(CRope), POINTER(CMem), c_void_p, c_void_p, c_int32, c_void_p,
                                c_int, c_int32, POINTER(CCache), c_void_p, c_void_p, c_void_p,
@@ -353,3 +357,32 @@ def revisit(rope: Rope, mem: Memory, sel_off, sel_idx, p_txt, cache: Cache, cach
                             _stream(stream, mem.device))
     _check("prcr_revisit", st)
     return new_pos, next_pos, new_cache_len, slot_mapping
+
+
+def prefill_capture(rope: Rope, mem: Memory, layer: int, raw_k, raw_v, pos, n_tokens, vis_index,
+                    cache: Cache, cache_start, write_coords: bool = True, err=None, stream=None):
+    """One prefill layer, fused (prcr_prefill_capture): rotated K and V into the cache
+    at the prompt's position ids, raw rows of visual tokens into the memory."""
+    torch = _torch()
+    B, M, NL, H, D = mem.k.shape
+    cache.check_matches(mem)
+    _need(raw_k, "raw_k", mem.k.dtype, 4, mem.device)
+    _need(raw_v, "raw_v", mem.k.dtype, 4, mem.device)
+    if raw_k.shape != raw_v.shape or raw_k.shape[0] != B or tuple(raw_k.shape[2:]) != (H, D):
+        raise ValueError("raw_k/raw_v must be [B, S_src, H, D]")
+    S = raw_k.shape[1]
+    _need(pos, "pos", torch.int32, 3, mem.device)
+    _shape(pos, "pos", (B, S, 3))
+    _need(n_tokens, "n_tokens", torch.int32, 1, mem.device)
+    _shape(n_tokens, "n_tokens", (B,))
+    _need(vis_index, "vis_index", torch.int32, 2, mem.device)
+    _shape(vis_index, "vis_index", (B, S))
+    _need(cache_start, "cache_start", torch.int32, 1, mem.device)
+    _shape(cache_start, "cache_start", (B,))
+    _err(err, mem.device)
+    st = lib().prcr_prefill_capture(ctypes.byref(rope.to_c()), ctypes.byref(mem.to_c()), int(layer),
+                                    _ptr(raw_k), _ptr(raw_v), int(S), _ptr(pos), _ptr(n_tokens),
+                                    _ptr(vis_index), int(bool(write_coords)),
+                                    ctypes.byref(cache.to_c()), _ptr(cache_start), _ptr(err),
+                                    _stream(stream, mem.device))
+    _check("prcr_prefill_capture", st)

@@ -238,6 +238,68 @@ prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem, const
   return e == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
 }
 
+prcr_status prcr_prefill_capture(const prcr_rope *rope, const prcr_mem *mem, int32_t layer,
+                                 const void *raw_k, const void *raw_v, int32_t s_src,
+                                 const int32_t *pos, const int32_t *n_tokens,
+                                 const int32_t *vis_index, int32_t write_coords,
+                                 const prcr_cache *cache, const int32_t *cache_start,
+                                 int32_t *err_flag, hipStream_t stream) {
+  prcr_status st = check_rope(rope);
+  if (st != PRCR_OK) return st;
+  st = check_mem(mem, write_coords != 0);
+  if (st != PRCR_OK) return st;
+  if (rope->head_dim != mem->head_dim) return PRCR_ERR_SHAPE;
+  if (raw_k == nullptr || raw_v == nullptr || pos == nullptr || n_tokens == nullptr ||
+      vis_index == nullptr || cache == nullptr || cache->k == nullptr || cache->v == nullptr ||
+      cache_start == nullptr)
+    return PRCR_ERR_NULL;
+  if (layer < 0 || layer >= mem->n_layers || s_src < 1) return PRCR_ERR_SHAPE;
+  if (cache->paged != 0 && cache->paged != 1) return PRCR_ERR_SHAPE;
+  if (cache->paged) {
+    if (cache->block_table == nullptr) return PRCR_ERR_NULL;
+    if (cache->block_size < 1 || cache->max_blocks < 1 || cache->n_blocks < 1) return PRCR_ERR_SHAPE;
+    if (!aligned(cache->block_table, 4)) return PRCR_ERR_ALIGN;
+  } else if (cache->s_max < 1) {
+    return PRCR_ERR_SHAPE;
+  }
+  if (!aligned(raw_k, 16) || !aligned(raw_v, 16) || !aligned(pos, 4) || !aligned(n_tokens, 4) ||
+      !aligned(vis_index, 4) || !aligned(cache->k, 16) || !aligned(cache->v, 16) ||
+      !aligned(cache_start, 4) || (err_flag != nullptr && !aligned(err_flag, 4)))
+    return PRCR_ERR_ALIGN;
+  const AxisMapId map = axis_map_id(*rope);
+  if (map == AxisMapId::kUnsupported) return PRCR_ERR_UNSUPPORTED;
+  PrefillParams p{};
+  p.raw_k = raw_k;
+  p.raw_v = raw_v;
+  p.pos = pos;
+  p.n_tokens = n_tokens;
+  p.vis_index = vis_index;
+  p.mem_k = mem->k;
+  p.mem_v = mem->v;
+  p.coords = mem->coords;
+  p.n_visual = mem->n_visual;
+  p.cache_k = cache->k;
+  p.cache_v = cache->v;
+  p.block_table = cache->block_table;
+  p.cache_start = cache_start;
+  p.err = err_flag;
+  p.batch = mem->batch;
+  p.s_src = s_src;
+  p.max_visual = mem->max_visual;
+  p.n_layers = mem->n_layers;
+  p.n_kv_heads = mem->n_kv_heads;
+  p.layer = layer;
+  p.write_coords = write_coords != 0;
+  p.s_max = cache->s_max;
+  p.block_size = cache->block_size;
+  p.max_blocks = cache->max_blocks;
+  p.n_blocks = cache->n_blocks;
+  for (int i = 0; i < rope->head_dim / 2; ++i)
+    p.inv_freq[i] = std::pow(rope->theta, -(2.0 * i) / rope->head_dim);
+  const hipError_t e = launch_prefill(p, mem->dtype, mem->head_dim, map, cache->paged != 0, stream);
+  return e == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
+}
+
 prcr_status prcr_revisit(const prcr_rope *rope, const prcr_mem *mem, const int32_t *sel_off,
                          const int32_t *sel_idx, int32_t total_k, const int32_t *p_txt,
                          prcr_mode mode, int32_t l_ext, const prcr_cache *cache,

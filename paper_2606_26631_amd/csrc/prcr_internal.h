@@ -88,6 +88,26 @@ struct StoreParams {
   int32_t row_bytes;              // n_kv_heads * head_dim * element size
 };
 
+struct PrefillParams {
+  const void *raw_k;
+  const void *raw_v;
+  const int32_t *pos;             // [batch][s_src][3] position ids
+  const int32_t *n_tokens;        // [batch]
+  const int32_t *vis_index;       // [batch][s_src], -1 for non-visual rows
+  void *mem_k;
+  void *mem_v;
+  int32_t *coords;
+  const int32_t *n_visual;
+  void *cache_k;
+  void *cache_v;
+  const int32_t *block_table;
+  const int32_t *cache_start;     // [batch]
+  int32_t *err;
+  int32_t batch, s_src, max_visual, n_layers, n_kv_heads, layer, write_coords;
+  int32_t s_max, block_size, max_blocks, n_blocks;
+  double inv_freq[kMaxPairs];
+};
+
 // Axis-map identifiers understood by the dispatcher.
 enum class AxisMapId : int {
   kS_8_12_12 = 0,
@@ -106,5 +126,7 @@ hipError_t launch_reassign(const ReassignParams &p, hipStream_t stream);
 hipError_t launch_rebind(const RebindParams &p, prcr_dtype dtype, int head_dim, AxisMapId map,
                          bool paged, bool fused, hipStream_t stream);
 hipError_t launch_store(const StoreParams &p, hipStream_t stream);
+hipError_t launch_prefill(const PrefillParams &p, prcr_dtype dtype, int head_dim, AxisMapId map,
+                          bool paged, hipStream_t stream);
 
 }  // namespace prcr

@@ -1,0 +1,181 @@
+// Prefill capture fused with rotary (the step before a revisit): for one layer,
+// read each prompt token's pre-rotary K/V rows once and
+//   * write the rotated key and the value into the standard decoder cache at the
+//     token's original position ids, Eq. (4), and
+//   * for visual tokens, write the raw rows into the Raw Visual Evidence Memory,
+//     Eq. (6)-(7) (optionally with the token's coordinates).
+//
+// One wavefront covers 2 x (rows per iteration) consecutive (sequence, token,
+// head) rows of the layer; a lane owns one 16-byte chunk of each half of a row,
+// as in the rebind kernel, and evaluates the cos/sin of its own pairs.
+#include <climits>
+#include <cmath>
+
+#include "prcr_internal.h"
+#include "rotary.h"
+
+namespace prcr {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kIters = 2;
+
+template <typename T, int D, class Map, bool kPaged>
+__global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const PrefillParams p) {
+  constexpr int P = D / 2;
+  constexpr int E = Store<T>::kPerChunk;
+  constexpr int LPR = P / E;
+  constexpr int RPI = kWave / LPR;
+  constexpr int kRowBytes = D * static_cast<int>(sizeof(T));
+  constexpr int kHalfBytes = kRowBytes / 2;
+  static_assert(Map::kPairs == P, "axis map does not match head_dim");
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int H = p.n_kv_heads;
+  const int64_t rows_all = static_cast<int64_t>(p.batch) * p.s_src * H;
+  const int64_t base = (static_cast<int64_t>(blockIdx.x) * kWaves + wave) * (RPI * kIters);
+  if (base >= rows_all) return;
+  const int r = lane / LPR;
+  const int c = lane % LPR;
+
+  // Row metadata and loads for both iterations first.
+  u32x4 kl[kIters], kh[kIters], vl[kIters], vh[kIters];
+  int rb[kIters], rs[kIters], rh[kIters];
+  bool live[kIters];
+#pragma unroll
+  for (int u = 0; u < kIters; ++u) {
+    const int64_t R = base + u * RPI + r;
+    live[u] = R < rows_all;
+    const int64_t Rc = live[u] ? R : 0;
+    rb[u] = static_cast<int>(Rc / (static_cast<int64_t>(p.s_src) * H));
+    const int64_t rem = Rc - static_cast<int64_t>(rb[u]) * p.s_src * H;
+    rs[u] = static_cast<int>(rem / H);
+    rh[u] = static_cast<int>(rem - static_cast<int64_t>(rs[u]) * H);
+    const int nt = p.n_tokens[rb[u]];
+    if (live[u] && (nt < 0 || nt > p.s_src) && rs[u] == 0 && rh[u] == 0 && c == 0 && p.err)
+      atomicOr(p.err, PRCR_DERR_INDEX);
+    live[u] = live[u] && rs[u] < min(max(nt, 0), p.s_src);
+    if (live[u]) {
+      const size_t o = static_cast<size_t>(Rc) * kRowBytes + c * 16;
+      kl[u] = load_nt(static_cast<const char *>(p.raw_k) + o);
+      kh[u] = load_nt(static_cast<const char *>(p.raw_k) + o + kHalfBytes);
+      vl[u] = load_nt(static_cast<const char *>(p.raw_v) + o);
+      vh[u] = load_nt(static_cast<const char *>(p.raw_v) + o + kHalfBytes);
+    }
+  }
+
+#pragma unroll
+  for (int u = 0; u < kIters; ++u) {
+    if (!live[u]) continue;
+    const int b = rb[u], s = rs[u], h = rh[u];
+    const int64_t tok = static_cast<int64_t>(b) * p.s_src + s;
+    const int32_t *pp = p.pos + 3 * tok;
+    const double pt = pp[0], ph = pp[1], pw = pp[2];
+
+    // Standard cache: rotated key and value at slot cache_start[b] + s (Eq. (4)).
+    const int64_t slot = static_cast<int64_t>(p.cache_start[b]) + s;
+    int64_t d = -1;
+    int flag = 0;
+    if constexpr (kPaged) {
+      const int64_t lb = slot >= 0 ? slot / p.block_size : -1;
+      if (lb < 0 || lb >= p.max_blocks) {
+        flag = PRCR_DERR_CAPACITY;
+      } else {
+        const int64_t blk = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
+        if (blk < 0 || blk >= p.n_blocks) {
+          flag = PRCR_DERR_BLOCK;
+        } else {
+          const int64_t off = slot - lb * p.block_size;
+          d = ((static_cast<int64_t>(p.layer) * p.n_blocks + blk) * p.block_size + off) * H + h;
+        }
+      }
+    } else {
+      if (slot < 0 || slot >= p.s_max)
+        flag = PRCR_DERR_CAPACITY;
+      else
+        d = ((static_cast<int64_t>(b) * p.n_layers + p.layer) * H + h) * p.s_max + slot;
+    }
+    if (d >= 0) {
+      double cs[E], sn[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int pair = c * E + e;
+        const int ax = Map::axis(pair);
+        sincos((ax == 0 ? pt : (ax == 1 ? ph : pw)) * p.inv_freq[pair], &sn[e], &cs[e]);
+      }
+      u32x4 ol, oh;
+      Store<T>::rotate(kl[u], kh[u], cs, sn, ol, oh);
+      char *ck = static_cast<char *>(p.cache_k) + d * kRowBytes + c * 16;
+      char *cv = static_cast<char *>(p.cache_v) + d * kRowBytes + c * 16;
+      store_nt(ck, ol);
+      store_nt(ck + kHalfBytes, oh);
+      store_nt(cv, vl[u]);
+      store_nt(cv + kHalfBytes, vh[u]);
+    }
+
+    // Raw Visual Evidence Memory: raw rows of visual tokens (Eq. (6)-(7)).
+    const int m = p.vis_index[tok];
+    if (m >= 0) {
+      if (m >= p.max_visual || m >= p.n_visual[b]) {
+        flag |= PRCR_DERR_INDEX;
+      } else {
+        const size_t mo = (((static_cast<size_t>(b) * p.max_visual + m) * p.n_layers + p.layer) * H + h) *
+                              kRowBytes + c * 16;
+        char *mk = static_cast<char *>(p.mem_k) + mo;
+        char *mv = static_cast<char *>(p.mem_v) + mo;
+        store_nt(mk, kl[u]);
+        store_nt(mk + kHalfBytes, kh[u]);
+        store_nt(mv, vl[u]);
+        store_nt(mv + kHalfBytes, vh[u]);
+        if (p.write_coords && h == 0 && c == 0) {
+          int32_t *co = p.coords + (static_cast<int64_t>(b) * p.max_visual + m) * 3;
+          co[0] = pp[0];
+          co[1] = pp[1];
+          co[2] = pp[2];
+        }
+      }
+    }
+    if (flag != 0 && c == 0 && p.err != nullptr) atomicOr(p.err, flag);
+  }
+}
+
+template <typename T, int D, class Map, bool kPaged>
+hipError_t launch_one(const PrefillParams &p, hipStream_t stream) {
+  constexpr int LPR = (D / 2) / Store<T>::kPerChunk;
+  constexpr int RPI = kWave / LPR;
+  const int64_t rows_all = static_cast<int64_t>(p.batch) * p.s_src * p.n_kv_heads;
+  const int64_t per_block = static_cast<int64_t>(kWaves) * RPI * kIters;
+  int64_t blocks = (rows_all + per_block - 1) / per_block;
+  if (blocks < 1) blocks = 1;
+  if (blocks > INT32_MAX) return hipErrorInvalidConfiguration;
+  prefill_capture_kernel<T, D, Map, kPaged><<<dim3(static_cast<unsigned>(blocks)), kWaves * kWave, 0,
+                                              stream>>>(p);
+  return hipGetLastError();
+}
+
+template <typename T, bool kPaged>
+hipError_t dispatch_map(const PrefillParams &p, int head_dim, AxisMapId map, hipStream_t stream) {
+  if (head_dim == 64) {
+    if (map == AxisMapId::kS_8_12_12) return launch_one<T, 64, Sectioned<8, 12, 12>, kPaged>(p, stream);
+    if (map == AxisMapId::kI_11_11_10) return launch_one<T, 64, Interleaved<11, 11, 10>, kPaged>(p, stream);
+  } else if (head_dim == 128) {
+    if (map == AxisMapId::kS_16_24_24) return launch_one<T, 128, Sectioned<16, 24, 24>, kPaged>(p, stream);
+    if (map == AxisMapId::kI_22_21_21) return launch_one<T, 128, Interleaved<22, 21, 21>, kPaged>(p, stream);
+    if (map == AxisMapId::kI_24_20_20) return launch_one<T, 128, Interleaved<24, 20, 20>, kPaged>(p, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_prefill(const PrefillParams &p, prcr_dtype dtype, int head_dim, AxisMapId map,
+                          bool paged, hipStream_t stream) {
+  if (dtype == PRCR_F32)
+    return paged ? dispatch_map<float, true>(p, head_dim, map, stream)
+                 : dispatch_map<float, false>(p, head_dim, map, stream);
+  return paged ? dispatch_map<uint16_t, true>(p, head_dim, map, stream)
+               : dispatch_map<uint16_t, false>(p, head_dim, map, stream);
+}
+
+}  // namespace prcr

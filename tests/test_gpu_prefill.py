@@ -1,0 +1,153 @@
+"""GPU parity of the fused prefill capture (prcr_prefill_capture) against the
+oracle, and the end-to-end property that a revisit at the original coordinates
+(IDENTITY reassignment) reproduces the keys the prefill wrote, bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_26631_amd as prcr
+import workloads
+from gpu_util import DEV, assert_keys_close, to_dev
+
+pytestmark = pytest.mark.gpu
+
+MAPS = [("f32", 64, (8, 12, 12), False), ("bf16", 128, (16, 24, 24), False),
+        ("bf16", 128, (24, 20, 20), True), ("f32", 128, (22, 21, 21), True)]
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+class Prefill:
+    def __init__(self, dtype, D, sections, inter, paged, NL=3, H=3, seed=5):
+        self.pos, self.vis_index, self.n_tokens, self.n_visual = workloads.prompt()
+        B, S = self.vis_index.shape
+        M = int(self.n_visual.max()) + 2
+        self.B, self.S, self.M, self.NL, self.H, self.D, self.dtype = B, S, M, NL, H, D, dtype
+        self.rope = {"head_dim": D, "sections": sections, "interleaved": inter,
+                     "theta": 5e6 if inter else 1e6}
+        g = torch.Generator().manual_seed(seed)
+        tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+        rnd = lambda *shape: torch.randn(shape, generator=g).to(tdt)
+        self.raw = [(rnd(B, S, H, D), rnd(B, S, H, D)) for _ in range(NL)]
+        self.mem_k = torch.zeros((B, M, NL, H, D), dtype=tdt)
+        self.mem_v = torch.zeros_like(self.mem_k)
+        self.paged = paged
+        if paged:
+            bs = 4
+            need = [(int(n) + 16 + bs - 1) // bs for n in self.n_tokens]
+            rng = np.random.default_rng(seed)
+            table = np.full((B, max(need)), -1, np.int32)
+            perm = rng.permutation(sum(need)).astype(np.int32)
+            o = 0
+            for b, n in enumerate(need):
+                table[b, :n] = perm[o:o + n]
+                o += n
+            self.cache_cfg = {"paged": True, "block_size": bs, "block_table": table,
+                              "max_blocks": max(need), "n_blocks": sum(need)}
+            shape = (NL, sum(need), bs, H, D)
+        else:
+            self.cache_cfg = {"paged": False, "s_max": S + 16}
+            shape = (B, NL, H, S + 16, D)
+        self.cache_k, self.cache_v = rnd(*shape), rnd(*shape)
+
+    def run_gpu(self, vis_index=None, start=None):
+        vis = self.vis_index if vis_index is None else vis_index
+        st = np.zeros(self.B, np.int32) if start is None else np.asarray(start, np.int32)
+        mem = prcr.Memory(self.mem_k.to(DEV), self.mem_v.to(DEV),
+                          torch.zeros((self.B, self.M, 3), dtype=torch.int32, device=DEV),
+                          to_dev(self.n_visual))
+        cache = prcr.Cache(self.cache_k.to(DEV), self.cache_v.to(DEV),
+                           to_dev(self.cache_cfg["block_table"]) if self.paged else None)
+        rope = prcr.Rope(self.D, self.rope["sections"], self.rope["interleaved"], self.rope["theta"])
+        err = torch.zeros(1, dtype=torch.int32, device=DEV)
+        for layer, (rk, rv) in enumerate(self.raw):
+            prcr.prefill_capture(rope, mem, layer, rk.to(DEV), rv.to(DEV), to_dev(self.pos),
+                                 to_dev(self.n_tokens), to_dev(vis), cache, to_dev(st), err=err)
+        torch.cuda.synchronize()
+        return mem, cache, rope, int(err.item())
+
+    def run_oracle(self, vis_index=None, start=None):
+        vis = self.vis_index if vis_index is None else vis_index
+        st = np.zeros(self.B, np.int64) if start is None else np.asarray(start, np.int64)
+        npy = workloads.as_numpy_storage
+        mem = {"k": npy(self.mem_k), "v": npy(self.mem_v), "coords": np.zeros((self.B, self.M, 3), np.int32),
+               "n_visual": self.n_visual, "dtype": self.dtype}
+        cache = dict(self.cache_cfg, k=npy(self.cache_k), v=npy(self.cache_v))
+        err = 0
+        for layer, (rk, rv) in enumerate(self.raw):
+            out = oracle.prefill_capture(self.rope, mem, layer, npy(rk), npy(rv), self.pos, self.n_tokens,
+                                         vis, True, cache, st)
+            err |= out["err"]
+            mem = dict(mem, k=out["mem_k"], v=out["mem_v"], coords=out["coords"])
+            cache = dict(cache, k=out["k"], v=out["v"])
+        return mem, cache, err
+
+
+def _compare(pf, mem, cache, err, ref_mem, ref_cache, ref_err):
+    npy = workloads.as_numpy_storage
+    assert err == ref_err
+    assert np.array_equal(npy(mem.k), ref_mem["k"]) and np.array_equal(npy(mem.v), ref_mem["v"])
+    assert np.array_equal(mem.coords.cpu().numpy(), ref_mem["coords"])
+    assert np.array_equal(npy(cache.v), ref_cache["v"])
+    gk = npy(cache.k)
+    same = gk == ref_cache["k"]
+    if not same.all():
+        rows = ~np.all(same, axis=-1)
+        assert_keys_close(gk[rows], ref_cache["k"][rows], pf.dtype)
+
+
+@pytest.mark.parametrize("paged", [False, True])
+@pytest.mark.parametrize("dtype,D,sections,inter", MAPS)
+def test_prefill_capture_parity(dtype, D, sections, inter, paged):
+    pf = Prefill(dtype, D, sections, inter, paged)
+    _say(f"prefill capture {dtype} D={D} {sections} inter={inter} paged={paged}")
+    mem, cache, rope, err = pf.run_gpu()
+    ref_mem, ref_cache, ref_err = pf.run_oracle()
+    _compare(pf, mem, cache, err, ref_mem, ref_cache, ref_err)
+
+
+def test_prefill_capture_errors():
+    pf = Prefill("bf16", 128, (16, 24, 24), False, False)
+    vis = pf.vis_index.copy()
+    vis[0, 6] = pf.M + 5                       # visual index outside the memory
+    _say("prefill capture with a bad visual index and a start past capacity")
+    mem, cache, rope, err = pf.run_gpu(vis, start=[0, 20])
+    ref_mem, ref_cache, ref_err = pf.run_oracle(vis, start=[0, 20])
+    assert ref_err == (oracle.ERR_INDEX | oracle.ERR_CAPACITY)
+    _compare(pf, mem, cache, err, ref_mem, ref_cache, ref_err)
+
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_identity_revisit_reproduces_prefill_keys(paged):
+    """Prefill-capture every layer, then revisit visual tokens at their original
+    coordinates: the injected keys and values equal the prefill's rows bit for bit."""
+    pf = Prefill("bf16", 128, (16, 24, 24), False, paged, NL=4, H=4)
+    _say(f"prefill -> IDENTITY revisit round trip, paged={paged}")
+    mem, cache, rope, err = pf.run_gpu()
+    assert err == 0
+    sel = [np.array([0, 3, 7, 11, 23]), np.array([2, 5, 29])]
+    sel_off = np.array([0, 5, 8], np.int32)
+    sel_idx = np.concatenate(sel).astype(np.int32)
+    p_txt = (pf.n_tokens - 1).astype(np.int32)
+    err_t = torch.zeros(1, dtype=torch.int32, device=DEV)
+    _, _, _, slots = prcr.revisit(rope, mem, to_dev(sel_off), to_dev(sel_idx), to_dev(p_txt), cache,
+                                  to_dev(pf.n_tokens), "identity", 2, err=err_t)
+    torch.cuda.synchronize()
+    assert int(err_t.item()) == 0
+    slots = slots.cpu().numpy()
+    for b in range(2):
+        for j, m in enumerate(sel[b]):
+            s_orig = int(np.nonzero(pf.vis_index[b] == m)[0][0])
+            new = int(slots[sel_off[b] + j])
+            if paged:
+                bs, t = pf.cache_cfg["block_size"], pf.cache_cfg["block_table"]
+                a = (slice(None), int(t[b][s_orig // bs]), s_orig % bs)
+                c = (slice(None), new // bs, new % bs)
+            else:
+                a = (b, slice(None), slice(None), s_orig)
+                c = (new // pf.cache_cfg["s_max"], slice(None), slice(None), new % pf.cache_cfg["s_max"])
+            assert torch.equal(cache.k[a].view(torch.int16), cache.k[c].view(torch.int16))
+            assert torch.equal(cache.v[a].view(torch.int16), cache.v[c].view(torch.int16))

@@ -331,3 +331,42 @@ def paper_k(model: str, K: int, seed: int = 2000) -> Workload:
                     True, 5e6, coords, np.array([M], np.int32), off, idx,
                     (lens - 1).astype(np.int32), lens, s_max=1024 + K, revisits=[(off, idx)],
                     seed=seed + K)
+
+
+def prompt(B=2, n_before=(5, 9), grid=((4, 6), (3, 5)), n_after=(3, 0), frames=(1, 2)):
+    """Prompt layout of a multimodal prefill: text, one image (or video) of grid
+    (gh, gw) x frames, text.  Position ids follow the M-RoPE convention: a text
+    token at p is (p, p, p); the image starts at the current text offset q with
+    (q + t, q + h, q + w); text resumes at 1 + the largest image position id.
+    Returns pos int32 [B][S][3], vis_index int32 [B][S] (visual index m or -1),
+    n_tokens int32 [B], n_visual int32 [B]."""
+    rows = []
+    for b in range(B):
+        gh, gw = grid[b]
+        tk = []
+        vis = []
+        q = 0
+        for _ in range(n_before[b]):
+            tk.append((q, q, q)); vis.append(-1); q += 1
+        m = 0
+        top = q
+        for t in range(frames[b]):
+            for h in range(gh):
+                for w in range(gw):
+                    tk.append((q + t, q + h, q + w)); vis.append(m); m += 1
+                    top = max(top, q + t, q + h, q + w)
+        q = top + 1
+        for _ in range(n_after[b]):
+            tk.append((q, q, q)); vis.append(-1); q += 1
+        rows.append((tk, vis, m))
+    S = max(len(r[0]) for r in rows)
+    pos = np.zeros((B, S, 3), np.int32)
+    vis_index = np.full((B, S), -1, np.int32)
+    n_tokens = np.zeros(B, np.int32)
+    n_visual = np.zeros(B, np.int32)
+    for b, (tk, vis, m) in enumerate(rows):
+        pos[b, :len(tk)] = tk
+        vis_index[b, :len(vis)] = vis
+        n_tokens[b] = len(tk)
+        n_visual[b] = m
+    return pos, vis_index, n_tokens, n_visual
