@@ -287,6 +287,59 @@ def prefill_capture_bw(dev, steps=20):
             "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4)}
 
 
+def decode_attention_bw(dev, steps=20):
+    """Bandwidth of decode attention over workload 3's active cache after its revisit
+    (32 sequences, lengths + 256, 36 layers x 8 KV heads, 32 query heads, d 128,
+    bf16), one layer per call.  Algorithmic bytes: every attended K and V row once,
+    plus the queries and outputs."""
+    import numpy as np
+    import torch
+
+    import paper_2606_26631_amd as prcr
+    import workloads
+    w = workloads.make(3, "full")
+    Hq = 4 * w.H
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(4000)
+    shape = (w.B, w.NL, w.H, w.s_max, w.D)
+    cache = prcr.Cache(torch.randn(shape, generator=g, device=dev).to(torch.bfloat16),
+                       torch.randn(shape, generator=g, device=dev).to(torch.bfloat16))
+    rope = prcr.Rope(w.D, w.sections, w.interleaved, w.theta)
+    lens = (w.cache_len + np.diff(w.sel_off)).astype(np.int32)
+    q = torch.randn((w.B, Hq, w.D), generator=g, device=dev).to(torch.bfloat16)
+    q_pos, cl = t(w.p_txt + 1), t(lens)
+    out = torch.empty((w.B, Hq, w.D), dtype=torch.float32, device=dev)
+    ws = torch.empty(prcr.decode_workspace_bytes(cache, w.B, Hq) // 4 + 1, dtype=torch.float32,
+                     device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    s = torch.cuda.Stream(device=dev)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        for layer in range(3):
+            prcr.decode_attention(rope, cache, layer, q, q_pos, cl, None, out, ws, err, s)
+        evs = []
+        for i in range(steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(s)
+            prcr.decode_attention(rope, cache, i % w.NL, q, q_pos, cl, None, out, ws, err, s)
+            b.record(s)
+            evs.append((a, b))
+        torch.cuda.synchronize()
+    if int(err.item()) != 0:
+        raise RuntimeError("device reported a data error in the decode attention runs")
+    ms = [a.elapsed_time(b) for a, b in evs]
+    mean_s = sum(ms) / len(ms) / 1e3
+    nbytes = int(lens.sum()) * w.H * w.D * 2 * 2 + w.B * Hq * w.D * (2 + 4)
+    del cache, ws
+    torch.cuda.empty_cache()
+    return {"kernel": "prcr_decode_attention", "workload": f"{w.B} sequences, cache lengths "
+            f"{int(lens.min())}-{int(lens.max())}, {w.H} KV heads, {Hq} query heads, d {w.D}, bf16, "
+            "one layer per call", "mean_call_us": round(mean_s * 1e6, 2),
+            "algorithmic_bytes_per_call": nbytes, "achieved": round(nbytes / mean_s / 1e9, 1),
+            "unit": "GB/s", "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4)}
+
+
 def roofline(w, rebind_ms, traffic):
     mean_s = sum(rebind_ms) / len(rebind_ms) / 1e3
     gbs = w.algorithmic_bytes() / mean_s / 1e9
@@ -363,6 +416,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-small-k", action="store_true", help="skip the small-K latency section")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-capture section")
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode-attention section")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the rebinding path shards by sequence, KV head or "
@@ -404,6 +458,8 @@ def main():
         out["small_k_latency"] = small_k_latency(dev)
     if not args.no_prefill:
         out["prefill_capture"] = prefill_capture_bw(dev)
+    if not args.no_decode:
+        out["decode_attention"] = decode_attention_bw(dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, dev, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -53,6 +53,7 @@
 #ifndef PRCR_H
 #define PRCR_H
 
+#include <stddef.h>
 #include <stdint.h>
 #include <hip/hip_runtime_api.h>
 
@@ -245,6 +246,39 @@ prcr_status prcr_revisit(const prcr_rope *rope, const prcr_mem *mem,
                          double *new_pos, int32_t *next_pos,
                          int32_t *new_cache_len, int64_t *slot_mapping,
                          int32_t *err_flag, hipStream_t stream);
+
+/*
+ * prcr_decode_attention - one decode step of attention over the active cache of
+ * one layer (Eq. (14)): for each sequence b and query head qh,
+ *   out[b][qh] = softmax(scale * RoPE(q[b][qh], (p, p, p)) . K^T) V,
+ * p = q_pos[b], over the keys in slots 0 .. cache_len[b]-1 of KV head
+ * qh / (n_q_heads / n_kv_heads) (grouped-query attention, at most 8 query heads
+ * per KV head).  The next text position of Sec. 3.3 is such a (p, p, p).
+ *
+ *   cache         contiguous or paged, head_dim = rope->head_dim (64 or 128),
+ *                 element type dtype, n_layers / n_kv_heads / batch as given
+ *   q             [batch][n_q_heads][head_dim] raw (pre-rotary) queries, dtype
+ *   out           float32 [batch][n_q_heads][head_dim]
+ *   workspace     at least prcr_decode_workspace_size() bytes of device memory,
+ *                 owned by the caller (split-K partial results; no state is kept)
+ *   scale         usually 1/sqrt(head_dim)
+ * Scores and the softmax are accumulated in float32; the query is rotated in
+ * double and rounded to float32 once.  cache_len[b] = 0 gives out = 0.  A
+ * cache_len beyond the capacity is clamped with PRCR_DERR_CAPACITY; a block-table
+ * entry outside the pool skips its keys with PRCR_DERR_BLOCK.
+ */
+prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache,
+                                  prcr_dtype dtype, int32_t batch, int32_t n_layers,
+                                  int32_t n_kv_heads, int32_t layer,
+                                  const void *q, int32_t n_q_heads, const int32_t *q_pos,
+                                  const int32_t *cache_len, float scale, float *out,
+                                  void *workspace, size_t workspace_bytes,
+                                  int32_t *err_flag, hipStream_t stream);
+
+/* Workspace bytes prcr_decode_attention needs for this cache and shape (host). */
+prcr_status prcr_decode_workspace_size(const prcr_cache *cache, int32_t batch,
+                                       int32_t n_q_heads, int32_t n_kv_heads,
+                                       int32_t head_dim, size_t *bytes);
 
 /* Host helpers (no GPU work). */
 

@@ -15,6 +15,8 @@ What it computes (Position Rebinding Cache Reuse, Sec. 3 and Algorithm 1):
                          other reinsertion rules named in Sec. 3.2 / Table 2.
 * ``rotate_keys``      - RoPE rebinding of the raw keys at the new coordinates,
                          Eq. (12) (keys) with Eq. (4)'s rotation convention.
+* ``decode_attention`` - one decode step of attention over the active cache,
+                         Eq. (14), with the query at a text position.
 * ``rebind_inject``    - gather of the selected memory rows (Eq. (11)), key
                          rebinding and value reuse (Eq. (12)), concatenation into
                          the active cache (Eq. (13)), next text position.
@@ -417,3 +419,45 @@ def rebind_entry(rope: dict, mem: dict, b: int, m: int, layer: int, head: int, p
     """One rebound key row and its value row (storage dtype), for sampled checks."""
     y = rebind_row(rope, mem["k"][b, m, layer, head], mem["dtype"], pos)
     return y, np.array(mem["v"][b, m, layer, head], copy=True)
+
+
+# --------------------------------------------------------------------------
+# Decode attention over the active cache, Eq. (14)
+# --------------------------------------------------------------------------
+def cache_rows(cache: dict, layer: int, b: int, kv_head: int, n: int, which: str = "k"):
+    """Rows of slots 0..n-1 of sequence b, one layer and KV head (storage form)."""
+    t = cache[which]
+    if cache["paged"]:
+        bs = cache["block_size"]
+        return np.stack([t[layer, cache["block_table"][b, s // bs], s % bs, kv_head]
+                         for s in range(n)]) if n else t[layer, :0, 0, kv_head]
+    return t[b, layer, kv_head, :n]
+
+
+def decode_attention(rope: dict, cache: dict, layer: int, q, q_pos, cache_len, scale: float,
+                     dtype: str):
+    """out[b][qh] = softmax(scale * RoPE(q[b][qh], (p, p, p)) . K^T) V over the
+    cache_len[b] keys of KV head qh // G (grouped-query attention), in float64;
+    an empty cache gives zeros."""
+    D = rope["head_dim"]
+    invf = inv_freq(rope["theta"], D)
+    axis = pair_axis(D, rope["sections"], rope["interleaved"])
+    n_kv = cache["k"].shape[3] if cache["paged"] else cache["k"].shape[2]
+    B, Hq = q.shape[0], q.shape[1]
+    G = Hq // n_kv
+    out = np.zeros((B, Hq, D), dtype=np.float64)
+    for b in range(B):
+        n = int(cache_len[b])
+        if n == 0:
+            continue
+        p = np.full(3, float(q_pos[b]))
+        for kvh in range(n_kv):
+            K = storage_to_f64(cache_rows(cache, layer, b, kvh, n, "k"), dtype)
+            V = storage_to_f64(cache_rows(cache, layer, b, kvh, n, "v"), dtype)
+            for g in range(G):
+                qh = kvh * G + g
+                qr = rotate_keys(storage_to_f64(q[b, qh], dtype), p, invf, axis)
+                s = (K @ qr) * scale
+                w = np.exp(s - s.max())
+                out[b, qh] = (w / w.sum()) @ V
+    return out

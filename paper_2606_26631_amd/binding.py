@@ -79,6 +79,14 @@ def lib() -> ctypes.CDLL:
     L.prcr_prefill_capture.argtypes = [POINTER(CRope), POINTER(CMem), c_int32, c_void_p, c_void_p,
                                        c_int32, c_void_p, c_void_p, c_void_p, c_int32,
                                        POINTER(CCache), c_void_p, c_void_p, c_void_p]
+    L.prcr_decode_workspace_size.restype = c_int
+    L.prcr_decode_workspace_size.argtypes = [POINTER(CCache), c_int32, c_int32, c_int32, c_int32,
+                                             POINTER(ctypes.c_size_t)]
+    L.prcr_decode_attention.restype = c_int
+    L.prcr_decode_attention.argtypes = [POINTER(CRope), POINTER(CCache), c_int, c_int32, c_int32,
+                                        c_int32, c_int32, c_void_p, c_int32, c_void_p, c_void_p,
+                                        ctypes.c_float, c_void_p, c_void_p, ctypes.c_size_t, c_void_p,
+                                        c_void_p]
     L.prcr_revisit.restype = c_int
     L.prcr_revisit.argtypes = [POINTER(CRope), POINTER(CMem), c_void_p, c_void_p, c_int32, c_void_p,
                                c_int, c_int32, POINTER(CCache), c_void_p, c_void_p, c_void_p,
@@ -386,3 +394,61 @@ def prefill_capture(rope: Rope, mem: Memory, layer: int, raw_k, raw_v, pos, n_to
                                     ctypes.byref(cache.to_c()), _ptr(cache_start), _ptr(err),
                                     _stream(stream, mem.device))
     _check("prcr_prefill_capture", st)
+
+
+def _cache_dims(cache: Cache):
+    """(n_layers, n_kv_heads, head_dim) of a cache tensor."""
+    if cache.paged:
+        NL, _, _, H, D = cache.k.shape
+    else:
+        _, NL, H, _, D = cache.k.shape
+    return NL, H, D
+
+
+def decode_workspace_bytes(cache: Cache, batch: int, n_q_heads: int) -> int:
+    """Bytes of workspace prcr_decode_attention needs (prcr_decode_workspace_size)."""
+    NL, H, D = _cache_dims(cache)
+    out = ctypes.c_size_t(0)
+    _check("prcr_decode_workspace_size",
+           lib().prcr_decode_workspace_size(ctypes.byref(cache.to_c()), int(batch), int(n_q_heads),
+                                            int(H), int(D), ctypes.byref(out)))
+    return int(out.value)
+
+
+def decode_attention(rope: Rope, cache: Cache, layer: int, q, q_pos, cache_len, scale=None,
+                     out=None, workspace=None, err=None, stream=None):
+    """One decode step of attention over one layer of the cache (prcr_decode_attention).
+    q [B, Hq, D] raw queries; returns out float32 [B, Hq, D]."""
+    torch = _torch()
+    NL, H, D = _cache_dims(cache)
+    _need(q, "q", cache.k.dtype, 3, cache.device)
+    B, Hq = q.shape[0], q.shape[1]
+    if q.shape[2] != D:
+        raise ValueError("q head_dim differs from the cache's")
+    if cache.paged and cache.block_table.shape[0] != B:
+        raise ValueError("block_table must have one row per sequence")
+    if not cache.paged and cache.k.shape[0] != B:
+        raise ValueError("contiguous cache batch differs from q's")
+    _need(q_pos, "q_pos", torch.int32, 1, cache.device)
+    _shape(q_pos, "q_pos", (B,))
+    _need(cache_len, "cache_len", torch.int32, 1, cache.device)
+    _shape(cache_len, "cache_len", (B,))
+    if out is None:
+        out = torch.empty((B, Hq, D), dtype=torch.float32, device=cache.device)
+    _need(out, "out", torch.float32, 3, cache.device)
+    _shape(out, "out", (B, Hq, D))
+    need = decode_workspace_bytes(cache, B, Hq)
+    if workspace is None:
+        workspace = torch.empty((max(need, 4) + 3) // 4, dtype=torch.float32, device=cache.device)
+    _need(workspace, "workspace", None, None, cache.device)
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace needs {need} bytes")
+    _err(err, cache.device)
+    sc = float(D) ** -0.5 if scale is None else float(scale)
+    st = lib().prcr_decode_attention(ctypes.byref(rope.to_c()), ctypes.byref(cache.to_c()),
+                                     _dtype_code(cache.k), int(B), int(NL), int(H), int(layer),
+                                     _ptr(q), int(Hq), _ptr(q_pos), _ptr(cache_len), sc, _ptr(out),
+                                     _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                     _ptr(err), _stream(stream, cache.device))
+    _check("prcr_decode_attention", st)
+    return out

@@ -3,6 +3,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <cstddef>
 
 #include "prcr_internal.h"
 
@@ -297,6 +298,91 @@ prcr_status prcr_prefill_capture(const prcr_rope *rope, const prcr_mem *mem, int
   for (int i = 0; i < rope->head_dim / 2; ++i)
     p.inv_freq[i] = std::pow(rope->theta, -(2.0 * i) / rope->head_dim);
   const hipError_t e = launch_prefill(p, mem->dtype, mem->head_dim, map, cache->paged != 0, stream);
+  return e == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
+}
+
+static prcr_status decode_shape(const prcr_cache *cache, int32_t batch, int32_t n_q_heads,
+                               int32_t n_kv_heads, int32_t head_dim, int *chunk, int *n_split) {
+  if (cache == nullptr) return PRCR_ERR_NULL;
+  if (batch < 1 || batch > 65535 || n_kv_heads < 1 || n_kv_heads > 65535 || n_q_heads < 1 ||
+      n_q_heads % n_kv_heads != 0 || n_q_heads / n_kv_heads > 8 || n_q_heads > 65535)
+    return PRCR_ERR_SHAPE;
+  if (head_dim != 64 && head_dim != 128) return PRCR_ERR_UNSUPPORTED;
+  if (cache->paged != 0 && cache->paged != 1) return PRCR_ERR_SHAPE;
+  int64_t cap;
+  if (cache->paged) {
+    if (cache->block_size < 1 || cache->max_blocks < 1 || cache->n_blocks < 1) return PRCR_ERR_SHAPE;
+    cap = static_cast<int64_t>(cache->max_blocks) * cache->block_size;
+  } else {
+    if (cache->s_max < 1) return PRCR_ERR_SHAPE;
+    cap = cache->s_max;
+  }
+  if (cap > INT32_MAX) return PRCR_ERR_SHAPE;
+  *chunk = decode_chunk(cap, batch, n_kv_heads);
+  const int64_t ns = (cap + *chunk - 1) / *chunk;
+  if (ns > INT32_MAX) return PRCR_ERR_SHAPE;
+  *n_split = static_cast<int>(ns);
+  return PRCR_OK;
+}
+
+prcr_status prcr_decode_workspace_size(const prcr_cache *cache, int32_t batch, int32_t n_q_heads,
+                                       int32_t n_kv_heads, int32_t head_dim, size_t *bytes) {
+  if (bytes == nullptr) return PRCR_ERR_NULL;
+  int chunk = 0, n_split = 0;
+  const prcr_status st = decode_shape(cache, batch, n_q_heads, n_kv_heads, head_dim, &chunk, &n_split);
+  if (st != PRCR_OK) return st;
+  *bytes = static_cast<size_t>(batch) * n_q_heads * n_split * (head_dim + 2) * sizeof(float);
+  return PRCR_OK;
+}
+
+prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache, prcr_dtype dtype,
+                                  int32_t batch, int32_t n_layers, int32_t n_kv_heads, int32_t layer,
+                                  const void *q, int32_t n_q_heads, const int32_t *q_pos,
+                                  const int32_t *cache_len, float scale, float *out,
+                                  void *workspace, size_t workspace_bytes, int32_t *err_flag,
+                                  hipStream_t stream) {
+  prcr_status st = check_rope(rope);
+  if (st != PRCR_OK) return st;
+  if (dtype != PRCR_F32 && dtype != PRCR_BF16) return PRCR_ERR_DTYPE;
+  int chunk = 0, n_split = 0;
+  st = decode_shape(cache, batch, n_q_heads, n_kv_heads, rope->head_dim, &chunk, &n_split);
+  if (st != PRCR_OK) return st;
+  if (cache->k == nullptr || cache->v == nullptr || q == nullptr || q_pos == nullptr ||
+      cache_len == nullptr || out == nullptr || workspace == nullptr ||
+      (cache->paged && cache->block_table == nullptr))
+    return PRCR_ERR_NULL;
+  if (n_layers < 1 || layer < 0 || layer >= n_layers || !std::isfinite(scale)) return PRCR_ERR_SHAPE;
+  const size_t need = static_cast<size_t>(batch) * n_q_heads * n_split * (rope->head_dim + 2) * sizeof(float);
+  if (workspace_bytes < need) return PRCR_ERR_SHAPE;
+  if (!aligned(cache->k, 16) || !aligned(cache->v, 16) || !aligned(q, 16) || !aligned(q_pos, 4) ||
+      !aligned(cache_len, 4) || !aligned(out, 4) || !aligned(workspace, 4) ||
+      (cache->paged && !aligned(cache->block_table, 4)) || (err_flag != nullptr && !aligned(err_flag, 4)))
+    return PRCR_ERR_ALIGN;
+  DecodeParams p{};
+  p.q = q;
+  p.q_pos = q_pos;
+  p.cache_len = cache_len;
+  p.cache_k = cache->k;
+  p.cache_v = cache->v;
+  p.block_table = cache->block_table;
+  p.out = out;
+  p.ws = static_cast<float *>(workspace);
+  p.err = err_flag;
+  p.batch = batch;
+  p.n_layers = n_layers;
+  p.n_kv_heads = n_kv_heads;
+  p.n_q_heads = n_q_heads;
+  p.layer = layer;
+  p.s_max = cache->s_max;
+  p.block_size = cache->block_size;
+  p.max_blocks = cache->max_blocks;
+  p.n_blocks = cache->n_blocks;
+  p.chunk = chunk;
+  p.n_split = n_split;
+  p.scale = scale;
+  for (int i = 0; i < rope->head_dim / 2; ++i)
+    p.inv_freq[i] = std::pow(rope->theta, -(2.0 * i) / rope->head_dim);
+  const hipError_t e = launch_decode(p, dtype, rope->head_dim, cache->paged != 0, stream);
   return e == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
 }
 

@@ -1,0 +1,284 @@
+// Decode attention over the active cache (Eq. (14)): for each sequence and query
+// head, softmax(RoPE(q, p_next) K^T * scale) V over the cache_len[b] keys of one
+// layer, with grouped-query attention (n_q_heads = G * n_kv_heads, query head
+// qh reads KV head qh / G).  The query is a text token, so its three M-RoPE
+// positions are equal and the rotation is the 1-D one at p_next.
+//
+// Split-K flash decoding.  Kernel 1: one workgroup per (key chunk, KV head,
+// sequence) streams its keys and values once for all G query heads of the
+// group: a 16-byte chunk of a key row per lane, scores reduced across the lanes
+// of a row with shuffles, online softmax in float32.  The workgroup's key groups
+// are merged in LDS and one (max, sum, weighted V) partial per query head and
+// chunk is written to the caller's workspace.  Kernel 2 merges the chunks.
+#include <cfloat>
+#include <climits>
+#include <cmath>
+
+#include "prcr_internal.h"
+#include "rotary.h"
+
+namespace prcr {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kIters = 2;
+
+template <typename T>
+struct Elems;
+template <>
+struct Elems<float> {
+  static constexpr int kPerChunk = 4;
+  __device__ static __forceinline__ void unpack(u32x4 w, float *x) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) x[q] = __uint_as_float(w[q]);
+  }
+};
+template <>
+struct Elems<uint16_t> {
+  static constexpr int kPerChunk = 8;
+  __device__ static __forceinline__ void unpack(u32x4 w, float *x) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      x[2 * q] = __uint_as_float(w[q] << 16);
+      x[2 * q + 1] = __uint_as_float(w[q] & 0xFFFF0000u);
+    }
+  }
+};
+
+template <typename T, int D, int GT, bool kPaged>
+__global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const DecodeParams p) {
+  constexpr int EPL = Elems<T>::kPerChunk;   // elements per lane (one 16-byte chunk)
+  constexpr int LPK = D / EPL;               // lanes per key row
+  constexpr int KPW = kWave / LPK;           // key rows per wave per iteration
+  constexpr int KPB = kWaves * KPW;          // key rows per workgroup per iteration
+  constexpr int kRowBytes = D * static_cast<int>(sizeof(T));
+  constexpr int P = D / 2;
+  static_assert(LPK >= 2 && kWave % LPK == 0, "unsupported head_dim");
+  __shared__ float s_m[kWaves][GT];
+  __shared__ float s_l[kWaves][GT];
+  __shared__ float s_o[kWaves][GT][D];
+
+  const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int kg = lane / LPK;                 // key row slot within the wave
+  const int c = lane % LPK;                  // 16-byte chunk of the row
+  const int grp = wave * KPW + kg;           // key row slot within the workgroup
+  const int G = p.n_q_heads / p.n_kv_heads;
+
+  const int64_t cap = kPaged ? static_cast<int64_t>(p.max_blocks) * p.block_size : p.s_max;
+  int len = p.cache_len[b];
+  if (len < 0 || len > cap) {
+    if (split == 0 && kvh == 0 && threadIdx.x == 0 && p.err != nullptr)
+      atomicOr(p.err, PRCR_DERR_CAPACITY);
+    len = static_cast<int>(min(max(static_cast<int64_t>(len), int64_t{0}), cap));
+  }
+  const int j0 = split * p.chunk;
+  const int j1 = min(len, j0 + p.chunk);
+
+  // Rotated, scaled query chunk of every head of the group: the lane's elements
+  // e = c*EPL .. c*EPL+EPL-1 pair with e +/- D/2, which sits in chunk c +/- LPK/2.
+  float qv[GT][EPL];
+  {
+    const double pq = static_cast<double>(p.q_pos[b]);
+    const bool first = c < LPK / 2;
+    const int cp = first ? c + LPK / 2 : c - LPK / 2;
+    double cs[EPL], sn[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      const int i = (c * EPL + e) % P;
+      sincos(pq * p.inv_freq[i], &sn[e], &cs[e]);
+    }
+#pragma unroll
+    for (int g = 0; g < GT; ++g) {
+      const int qh = kvh * G + (g < G ? g : 0);
+      const char *qrow = static_cast<const char *>(p.q) + (static_cast<int64_t>(b) * p.n_q_heads + qh) * kRowBytes;
+      float x[EPL], xp[EPL];
+      Elems<T>::unpack(*reinterpret_cast<const u32x4 *>(qrow + c * 16), x);
+      Elems<T>::unpack(*reinterpret_cast<const u32x4 *>(qrow + cp * 16), xp);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        const double y = first ? static_cast<double>(x[e]) * cs[e] - static_cast<double>(xp[e]) * sn[e]
+                               : static_cast<double>(x[e]) * cs[e] + static_cast<double>(xp[e]) * sn[e];
+        qv[g][e] = static_cast<float>(y * p.scale);
+      }
+    }
+  }
+
+  float m[GT], l[GT], o[GT][EPL];
+#pragma unroll
+  for (int g = 0; g < GT; ++g) {
+    m[g] = -FLT_MAX;
+    l[g] = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) o[g][e] = 0.f;
+  }
+
+  const int64_t row_base = kPaged ? 0
+                                  : ((static_cast<int64_t>(b) * p.n_layers + p.layer) * p.n_kv_heads + kvh) * p.s_max;
+  int bad_block = 0;
+  for (int jb = j0; jb < j1; jb += KPB * kIters) {
+    u32x4 kc[kIters], vc[kIters];
+    bool live[kIters];
+#pragma unroll
+    for (int u = 0; u < kIters; ++u) {
+      const int j = jb + u * KPB + grp;
+      live[u] = j < j1;
+      if (live[u]) {
+        int64_t row;
+        if constexpr (kPaged) {
+          const int64_t blk = p.block_table[static_cast<int64_t>(b) * p.max_blocks + j / p.block_size];
+          if (blk < 0 || blk >= p.n_blocks) {
+            live[u] = false;
+            bad_block = 1;
+            continue;
+          }
+          row = ((static_cast<int64_t>(p.layer) * p.n_blocks + blk) * p.block_size + j % p.block_size) *
+                    p.n_kv_heads + kvh;
+        } else {
+          row = row_base + j;
+        }
+        kc[u] = load_nt(static_cast<const char *>(p.cache_k) + row * kRowBytes + c * 16);
+        vc[u] = load_nt(static_cast<const char *>(p.cache_v) + row * kRowBytes + c * 16);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kIters; ++u) {
+      float k[EPL], v[EPL];
+      Elems<T>::unpack(kc[u], k);
+      Elems<T>::unpack(vc[u], v);
+#pragma unroll
+      for (int g = 0; g < GT; ++g) {
+        float s = 0.f;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) s = fmaf(qv[g][e], k[e], s);
+#pragma unroll
+        for (int off = LPK / 2; off > 0; off >>= 1) s += __shfl_xor(s, off);
+        if (live[u] && g < G) {
+          const float mn = fmaxf(m[g], s);
+          const float corr = __expf(m[g] - mn);
+          const float pj = __expf(s - mn);
+          l[g] = l[g] * corr + pj;
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) o[g][e] = o[g][e] * corr + pj * v[e];
+          m[g] = mn;
+        }
+      }
+    }
+  }
+  if (bad_block && p.err != nullptr && c == 0) atomicOr(p.err, PRCR_DERR_BLOCK);
+
+  // Merge the wave's key-row slots (lanes LPK apart hold the same elements of
+  // different slots), then the workgroup's waves in LDS, and write this chunk's
+  // partials.  Empty slots carry l = 0 and o = 0, so their weight is harmless.
+#pragma unroll
+  for (int off = LPK; off < kWave; off <<= 1) {
+#pragma unroll
+    for (int g = 0; g < GT; ++g) {
+      const float m2 = __shfl_xor(m[g], off);
+      const float l2 = __shfl_xor(l[g], off);
+      const float mx = fmaxf(m[g], m2);
+      const float w1 = __expf(m[g] - mx), w2 = __expf(m2 - mx);
+      l[g] = l[g] * w1 + l2 * w2;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) o[g][e] = o[g][e] * w1 + __shfl_xor(o[g][e], off) * w2;
+      m[g] = mx;
+    }
+  }
+  if (kg == 0) {
+#pragma unroll
+    for (int g = 0; g < GT; ++g) {
+      if (c == 0) {
+        s_m[wave][g] = m[g];
+        s_l[wave][g] = l[g];
+      }
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) s_o[wave][g][c * EPL + e] = o[g][e];
+    }
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < G * D; idx += kWaves * kWave) {
+    const int g = idx / D, d = idx % D;
+    float M = -FLT_MAX;
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][g]);
+    float Ls = 0.f, Os = 0.f;
+    for (int w = 0; w < kWaves; ++w) {
+      const float wt = __expf(s_m[w][g] - M);
+      Ls += s_l[w][g] * wt;
+      Os += s_o[w][g][d] * wt;
+    }
+    float *ws = p.ws + ((static_cast<int64_t>(b) * p.n_q_heads + kvh * G + g) * p.n_split + split) * (D + 2);
+    ws[d] = Os;
+    if (d == 0) {
+      ws[D] = M;
+      ws[D + 1] = Ls;
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(D) void decode_combine_kernel(const DecodeParams p) {
+  const int qh = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
+  const float *ws = p.ws + (static_cast<int64_t>(b) * p.n_q_heads + qh) * p.n_split * (D + 2);
+  float M = -FLT_MAX;
+  for (int s = 0; s < p.n_split; ++s)
+    if (ws[s * (D + 2) + D + 1] > 0.f) M = fmaxf(M, ws[s * (D + 2) + D]);
+  float Ls = 0.f, Os = 0.f;
+  for (int s = 0; s < p.n_split; ++s) {
+    const float l = ws[s * (D + 2) + D + 1];
+    if (l > 0.f) {
+      const float w = __expf(ws[s * (D + 2) + D] - M);
+      Ls += l * w;
+      Os += ws[s * (D + 2) + d] * w;
+    }
+  }
+  p.out[(static_cast<int64_t>(b) * p.n_q_heads + qh) * D + d] = Ls > 0.f ? Os / Ls : 0.f;
+}
+
+template <typename T, int D, int GT, bool kPaged>
+hipError_t launch_split(const DecodeParams &p, hipStream_t stream) {
+  decode_partial_kernel<T, D, GT, kPaged>
+      <<<dim3(p.n_split, p.n_kv_heads, p.batch), kWaves * kWave, 0, stream>>>(p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  decode_combine_kernel<D><<<dim3(p.n_q_heads, p.batch), D, 0, stream>>>(p);
+  return hipGetLastError();
+}
+
+template <typename T, int D, bool kPaged>
+hipError_t dispatch_group(const DecodeParams &p, int G, hipStream_t stream) {
+  if (G <= 1) return launch_split<T, D, 1, kPaged>(p, stream);
+  if (G <= 2) return launch_split<T, D, 2, kPaged>(p, stream);
+  if (G <= 4) return launch_split<T, D, 4, kPaged>(p, stream);
+  return launch_split<T, D, 8, kPaged>(p, stream);
+}
+
+template <typename T, bool kPaged>
+hipError_t dispatch_dim(const DecodeParams &p, int head_dim, int G, hipStream_t stream) {
+  if (head_dim == 64) return dispatch_group<T, 64, kPaged>(p, G, stream);
+  if (head_dim == 128) return dispatch_group<T, 128, kPaged>(p, G, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+int decode_chunk(int64_t capacity, int batch, int n_kv_heads) {
+  // About 2048 workgroups over the whole batch, chunks of 64..4096 keys.
+  const int64_t want = (capacity * batch * n_kv_heads + 2047) / 2048;
+  int64_t chunk = (want + 63) / 64 * 64;
+  if (chunk < 64) chunk = 64;
+  if (chunk > 4096) chunk = 4096;
+  return static_cast<int>(chunk);
+}
+
+hipError_t launch_decode(const DecodeParams &p, prcr_dtype dtype, int head_dim, bool paged,
+                         hipStream_t stream) {
+  const int G = p.n_q_heads / p.n_kv_heads;
+  if (dtype == PRCR_F32)
+    return paged ? dispatch_dim<float, true>(p, head_dim, G, stream)
+                 : dispatch_dim<float, false>(p, head_dim, G, stream);
+  return paged ? dispatch_dim<uint16_t, true>(p, head_dim, G, stream)
+               : dispatch_dim<uint16_t, false>(p, head_dim, G, stream);
+}
+
+}  // namespace prcr

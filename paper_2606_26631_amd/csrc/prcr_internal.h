@@ -108,6 +108,23 @@ struct PrefillParams {
   double inv_freq[kMaxPairs];
 };
 
+struct DecodeParams {
+  const void *q;                  // [batch][n_q_heads][head_dim]
+  const int32_t *q_pos;           // [batch]
+  const int32_t *cache_len;       // [batch]
+  const void *cache_k;
+  const void *cache_v;
+  const int32_t *block_table;
+  float *out;                     // [batch][n_q_heads][head_dim]
+  float *ws;                      // [batch][n_q_heads][n_split][head_dim + 2]
+  int32_t *err;
+  int32_t batch, n_layers, n_kv_heads, n_q_heads, layer;
+  int32_t s_max, block_size, max_blocks, n_blocks;
+  int32_t chunk, n_split;
+  float scale;
+  double inv_freq[kMaxPairs];
+};
+
 // Axis-map identifiers understood by the dispatcher.
 enum class AxisMapId : int {
   kS_8_12_12 = 0,
@@ -128,5 +145,8 @@ hipError_t launch_rebind(const RebindParams &p, prcr_dtype dtype, int head_dim, 
 hipError_t launch_store(const StoreParams &p, hipStream_t stream);
 hipError_t launch_prefill(const PrefillParams &p, prcr_dtype dtype, int head_dim, AxisMapId map,
                           bool paged, hipStream_t stream);
+hipError_t launch_decode(const DecodeParams &p, prcr_dtype dtype, int head_dim, bool paged,
+                         hipStream_t stream);
+int decode_chunk(int64_t capacity, int batch, int n_kv_heads);
 
 }  // namespace prcr

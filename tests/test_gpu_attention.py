@@ -1,0 +1,132 @@
+"""GPU parity of decode attention over the active cache (Eq. (14)) against the
+float64 oracle, and the whole path end to end: prefill capture -> PCR revisit ->
+decode attention.
+
+Tolerance (derived from the arithmetic): scores and the softmax are accumulated in
+float32 over at most a chunk of keys per lane group before the float32 merges, so
+|out - ref| <= 5e-5 * max |V| over the attended rows (+ 1e-6)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_26631_amd as prcr
+import workloads
+from gpu_util import DEV, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _check(out, ref, cache_o, lens, n_kv, G, dtype, layer):
+    out = out.cpu().numpy()
+    for b in range(len(lens)):
+        for kvh in range(n_kv):
+            n = int(lens[b])
+            vmax = np.abs(oracle.storage_to_f64(oracle.cache_rows(cache_o, layer, b, kvh, n, "v"),
+                                                dtype)).max() if n else 0.0
+            for g in range(G):
+                qh = kvh * G + g
+                d = np.abs(out[b, qh] - ref[b, qh]).max()
+                assert d <= 5e-5 * vmax + 1e-6, (b, qh, d, vmax)
+
+
+CASES = [("bf16", 128, 4, False), ("bf16", 128, 7, True), ("bf16", 128, 8, False),
+         ("bf16", 64, 2, True), ("f32", 64, 1, False), ("f32", 128, 4, True), ("bf16", 128, 1, True)]
+
+
+@pytest.mark.parametrize("dtype,D,G,paged", CASES)
+def test_decode_attention_parity(dtype, D, G, paged):
+    B, NL, H, layer = 4, 2, 2, 1
+    lens = np.array([0, 1, 700, 333], np.int32)
+    cap = 800
+    g = torch.Generator().manual_seed(D + G)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    rnd = lambda *s: torch.randn(s, generator=g).to(tdt)
+    rng = np.random.default_rng(G)
+    if paged:
+        bs = 16
+        need = (cap + bs - 1) // bs
+        table = rng.permutation(B * need).astype(np.int32).reshape(B, need)
+        k, v = rnd(NL, B * need, bs, H, D), rnd(NL, B * need, bs, H, D)
+        cache_o = {"paged": True, "block_size": bs, "block_table": table, "max_blocks": need,
+                   "n_blocks": B * need}
+    else:
+        k, v = rnd(B, NL, H, cap, D), rnd(B, NL, H, cap, D)
+        cache_o = {"paged": False, "s_max": cap}
+    cache_o["k"], cache_o["v"] = workloads.as_numpy_storage(k), workloads.as_numpy_storage(v)
+    q = rnd(B, H * G, D)
+    q_pos = rng.integers(0, 20000, B).astype(np.int32)
+    _say(f"decode attention {dtype} D={D} G={G} paged={paged}")
+    cache = prcr.Cache(k.to(DEV), v.to(DEV), to_dev(cache_o["block_table"]) if paged else None)
+    rope = prcr.Rope(D, (8, 12, 12) if D == 64 else (16, 24, 24), False, 1e6)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out = prcr.decode_attention(rope, cache, layer, q.to(DEV), to_dev(q_pos), to_dev(lens), err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    ref = oracle.decode_attention(rope.__dict__ | {"sections": rope.sections}, cache_o, layer,
+                                  workloads.as_numpy_storage(q), q_pos, lens, D ** -0.5, dtype)
+    _check(out, ref, cache_o, lens, H, G, dtype, layer)
+    assert not out[0].any()
+
+
+def test_decode_after_prefill_and_revisit():
+    """The path end to end on the GPU against the oracle: every layer's prefill
+    capture, a PCR revisit of selected visual tokens, then decode attention of the
+    next text token (Eq. (4), (6)-(14))."""
+    pos, vis, n_tok, n_vis = workloads.prompt()
+    B, S = vis.shape
+    NL, H, D, G = 3, 2, 128, 4
+    M = int(n_vis.max())
+    rope_d = {"head_dim": D, "sections": (24, 20, 20), "interleaved": True, "theta": 5e6}
+    g = torch.Generator().manual_seed(77)
+    raw = [(torch.randn((B, S, H, D), generator=g).to(torch.bfloat16),
+            torch.randn((B, S, H, D), generator=g).to(torch.bfloat16)) for _ in range(NL)]
+    s_max = S + 40
+    ck = torch.zeros((B, NL, H, s_max, D), dtype=torch.bfloat16)
+    cv = torch.zeros_like(ck)
+    mem = prcr.Memory(torch.zeros((B, M, NL, H, D), dtype=torch.bfloat16, device=DEV),
+                      torch.zeros((B, M, NL, H, D), dtype=torch.bfloat16, device=DEV),
+                      torch.zeros((B, M, 3), dtype=torch.int32, device=DEV), to_dev(n_vis))
+    cache = prcr.Cache(ck.to(DEV), cv.to(DEV))
+    rope = prcr.Rope(D, rope_d["sections"], True, rope_d["theta"])
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    zero = torch.zeros(B, dtype=torch.int32, device=DEV)
+    for layer, (rk, rv) in enumerate(raw):
+        prcr.prefill_capture(rope, mem, layer, rk.to(DEV), rv.to(DEV), to_dev(pos), to_dev(n_tok),
+                             to_dev(vis), cache, zero, err=err)
+    sel = [np.array([1, 4, 9, 10, 22]), np.array([0, 7, 29])]
+    sel_off = np.array([0, 5, 8], np.int32)
+    sel_idx = np.concatenate(sel).astype(np.int32)
+    p_txt = (pos[np.arange(B), n_tok - 1, 0]).astype(np.int32)        # latest text position
+    _, next_pos, new_len, _ = prcr.revisit(rope, mem, to_dev(sel_off), to_dev(sel_idx), to_dev(p_txt),
+                                           cache, to_dev(n_tok), "pcr", 2, err=err)
+    q = torch.randn((B, H * G, D), generator=g).to(torch.bfloat16)
+    outs = [prcr.decode_attention(rope, cache, layer, q.to(DEV), next_pos, new_len, err=err)
+            for layer in range(NL)]
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    _say("prefill -> revisit -> decode on the GPU done; running the oracle pipeline")
+
+    npy = workloads.as_numpy_storage
+    mem_o = {"k": np.zeros((B, M, NL, H, D), np.uint16), "v": np.zeros((B, M, NL, H, D), np.uint16),
+             "coords": np.zeros((B, M, 3), np.int32), "n_visual": n_vis, "dtype": "bf16"}
+    cache_o = {"paged": False, "s_max": s_max, "k": npy(ck), "v": npy(cv)}
+    for layer, (rk, rv) in enumerate(raw):
+        o = oracle.prefill_capture(rope_d, mem_o, layer, npy(rk), npy(rv), pos, n_tok, vis, True,
+                                   cache_o, np.zeros(B, np.int64))
+        mem_o = dict(mem_o, k=o["mem_k"], v=o["mem_v"], coords=o["coords"])
+        cache_o = dict(cache_o, k=o["k"], v=o["v"])
+    new_pos_o, next_o, e1 = oracle.reassign_batch(mem_o["coords"], n_vis, sel_off, sel_idx, p_txt)
+    res = oracle.rebind_inject(rope_d, mem_o, sel_off, sel_idx, new_pos_o, cache_o, n_tok)
+    assert e1 == 0 and res["err"] == 0
+    assert np.array_equal(next_pos.cpu().numpy(), next_o)
+    assert np.array_equal(new_len.cpu().numpy(), res["new_cache_len"])
+    cache_o = dict(cache_o, k=res["k"], v=res["v"])
+    for layer in range(NL):
+        ref = oracle.decode_attention(rope_d, cache_o, layer, npy(q), next_o, res["new_cache_len"],
+                                      D ** -0.5, "bf16")
+        _check(outs[layer], ref, cache_o, res["new_cache_len"], H, G, "bf16", layer)
