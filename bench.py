@@ -33,6 +33,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 KERNEL_SOURCES = ["paper_2606_26631_amd/csrc/rebind.hip", "paper_2606_26631_amd/csrc/reassign.hip",
+                  "paper_2606_26631_amd/csrc/rotary.h", "paper_2606_26631_amd/csrc/positions.h",
                   "paper_2606_26631_amd/csrc/prcr_internal.h", "paper_2606_26631_amd/csrc/api.cpp"]
 
 

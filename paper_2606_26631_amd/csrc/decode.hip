@@ -20,8 +20,14 @@
 namespace prcr {
 namespace {
 
+#ifndef PRCR_DEC_ITERS
+#define PRCR_DEC_ITERS 1
+#endif
+#ifndef PRCR_DEC_WORKGROUPS
+#define PRCR_DEC_WORKGROUPS 1024
+#endif
 constexpr int kWaves = 4;
-constexpr int kIters = 2;
+constexpr int kIters = PRCR_DEC_ITERS;   // key rows per lane group in flight
 
 template <typename T>
 struct Elems;
@@ -117,19 +123,21 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
   const int64_t row_base = kPaged ? 0
                                   : ((static_cast<int64_t>(b) * p.n_layers + p.layer) * p.n_kv_heads + kvh) * p.s_max;
   int bad_block = 0;
-  for (int jb = j0; jb < j1; jb += KPB * kIters) {
-    u32x4 kc[kIters], vc[kIters];
-    bool live[kIters];
+  // Loads of the next batch of key rows are issued before the current batch is
+  // scored, so one batch is always in flight.
+  u32x4 kc[kIters], vc[kIters];
+  bool live[kIters];
+  auto load_batch = [&](int jb, u32x4 *kd, u32x4 *vd, bool *lv) {
 #pragma unroll
     for (int u = 0; u < kIters; ++u) {
       const int j = jb + u * KPB + grp;
-      live[u] = j < j1;
-      if (live[u]) {
+      lv[u] = j < j1;
+      if (lv[u]) {
         int64_t row;
         if constexpr (kPaged) {
           const int64_t blk = p.block_table[static_cast<int64_t>(b) * p.max_blocks + j / p.block_size];
           if (blk < 0 || blk >= p.n_blocks) {
-            live[u] = false;
+            lv[u] = false;
             bad_block = 1;
             continue;
           }
@@ -138,10 +146,16 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
         } else {
           row = row_base + j;
         }
-        kc[u] = load_nt(static_cast<const char *>(p.cache_k) + row * kRowBytes + c * 16);
-        vc[u] = load_nt(static_cast<const char *>(p.cache_v) + row * kRowBytes + c * 16);
+        kd[u] = load_nt(static_cast<const char *>(p.cache_k) + row * kRowBytes + c * 16);
+        vd[u] = load_nt(static_cast<const char *>(p.cache_v) + row * kRowBytes + c * 16);
       }
     }
+  };
+  load_batch(j0, kc, vc, live);
+  for (int jb = j0; jb < j1; jb += KPB * kIters) {
+    u32x4 nk[kIters], nv[kIters];
+    bool nl[kIters];
+    load_batch(jb + KPB * kIters, nk, nv, nl);
 #pragma unroll
     for (int u = 0; u < kIters; ++u) {
       float k[EPL], v[EPL];
@@ -164,6 +178,12 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
           m[g] = mn;
         }
       }
+    }
+#pragma unroll
+    for (int u = 0; u < kIters; ++u) {
+      kc[u] = nk[u];
+      vc[u] = nv[u];
+      live[u] = nl[u];
     }
   }
   if (bad_block && p.err != nullptr && c == 0) atomicOr(p.err, PRCR_DERR_BLOCK);
@@ -263,8 +283,8 @@ hipError_t dispatch_dim(const DecodeParams &p, int head_dim, int G, hipStream_t 
 }  // namespace
 
 int decode_chunk(int64_t capacity, int batch, int n_kv_heads) {
-  // About 2048 workgroups over the whole batch, chunks of 64..4096 keys.
-  const int64_t want = (capacity * batch * n_kv_heads + 2047) / 2048;
+  // About PRCR_DEC_WORKGROUPS workgroups over the whole batch, chunks of 64..4096 keys.
+  const int64_t want = (capacity * batch * n_kv_heads + PRCR_DEC_WORKGROUPS - 1) / PRCR_DEC_WORKGROUPS;
   int64_t chunk = (want + 63) / 64 * 64;
   if (chunk < 64) chunk = 64;
   if (chunk > 4096) chunk = 4096;

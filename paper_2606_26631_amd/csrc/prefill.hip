@@ -17,8 +17,11 @@
 namespace prcr {
 namespace {
 
+#ifndef PRCR_PF_ITERS
+#define PRCR_PF_ITERS 1
+#endif
 constexpr int kWaves = 4;
-constexpr int kIters = 2;
+constexpr int kIters = PRCR_PF_ITERS;
 
 template <typename T, int D, class Map, bool kPaged>
 __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const PrefillParams p) {
@@ -38,8 +41,12 @@ __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const P
   if (base >= rows_all) return;
   const int r = lane / LPR;
   const int c = lane % LPR;
+  // With n_kv_heads a multiple of the rows per iteration, the RPI-aligned rows of
+  // an iteration are heads of one token: validity and slot are then uniform across
+  // the wave, and one sincos per lane shared by shuffles covers the token.
+  const bool one_token = (H % RPI) == 0;
 
-  // Row metadata and loads for both iterations first.
+  // Row metadata and loads for all iterations first.
   u32x4 kl[kIters], kh[kIters], vl[kIters], vh[kIters];
   int rb[kIters], rs[kIters], rh[kIters];
   bool live[kIters];
@@ -98,11 +105,25 @@ __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const P
     }
     if (d >= 0) {
       double cs[E], sn[E];
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const int pair = c * E + e;
+      if (one_token) {
+        // All rows of this iteration belong to one token: lane i evaluates pair i
+        // (mod P) and each lane gathers its E pairs with shuffles.
+        const int pair = lane % P;
         const int ax = Map::axis(pair);
-        sincos((ax == 0 ? pt : (ax == 1 ? ph : pw)) * p.inv_freq[pair], &sn[e], &cs[e]);
+        double sv, cv;
+        sincos((ax == 0 ? pt : (ax == 1 ? ph : pw)) * p.inv_freq[pair], &sv, &cv);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          cs[e] = __shfl(cv, c * E + e);
+          sn[e] = __shfl(sv, c * E + e);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int pair = c * E + e;
+          const int ax = Map::axis(pair);
+          sincos((ax == 0 ? pt : (ax == 1 ? ph : pw)) * p.inv_freq[pair], &sn[e], &cs[e]);
+        }
       }
       u32x4 ol, oh;
       Store<T>::rotate(kl[u], kh[u], cs, sn, ol, oh);
