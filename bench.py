@@ -32,14 +32,20 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-KERNEL_SOURCES = ["paper_2606_26631_amd/csrc/rebind.hip", "paper_2606_26631_amd/csrc/reassign.hip",
-                  "paper_2606_26631_amd/csrc/rotary.h", "paper_2606_26631_amd/csrc/positions.h",
-                  "paper_2606_26631_amd/csrc/prcr_internal.h", "paper_2606_26631_amd/csrc/api.cpp"]
+_CSRC = "paper_2606_26631_amd/csrc/"
+_COMMON = [_CSRC + f for f in ("rotary.h", "prcr_internal.h", "api.cpp")]
+# Sources each measured kernel is built from; a committed counter summary
+# applies only while their hash is the one it was taken on.
+KERNEL_SOURCES = {
+    "rebind": [_CSRC + "rebind.hip", _CSRC + "reassign.hip", _CSRC + "positions.h"] + _COMMON,
+    "prefill": [_CSRC + "prefill.hip"] + _COMMON,
+    "decode": [_CSRC + "decode.hip"] + _COMMON,
+}
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(kind: str = "rebind") -> str:
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in KERNEL_SOURCES[kind]:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -56,15 +62,16 @@ def describe(w) -> dict:
     return cfg
 
 
-def load_counters(w, khash):
-    """HBM traffic per launch from committed rocprofv3 counter summaries, if they
-    were taken on the current kernel sources; else None."""
-    path = os.path.join(ROOT, "profiles", f"counters_rebind_workload{w.cfg}.json")
+def load_traffic(name: str, kind: str):
+    """HBM bytes per launch from a committed rocprofv3 counter summary
+    (profiles/counters_<name>.json), if it was taken on the current sources of
+    that kernel; else None."""
+    path = os.path.join(ROOT, "profiles", f"counters_{name}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         c = json.load(f)
-    if c.get("kernel_source_hash") != khash:
+    if c.get("kernel_source_hash") != kernel_source_hash(kind):
         return None
     return c.get("traffic_bytes_per_launch")
 
@@ -285,7 +292,8 @@ def prefill_capture_bw(dev, steps=20):
             f"({int(n_vis[0])} visual), {NL} layers x {H} KV heads, d {D}, bf16, one layer per call",
             "mean_launch_us": round(mean_s * 1e6, 2), "algorithmic_bytes_per_call": nbytes,
             "achieved": round(nbytes / mean_s / 1e9, 1), "unit": "GB/s",
-            "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4)}
+            "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4),
+            "traffic": load_traffic("prefill_capture", "prefill")}
 
 
 def decode_attention_bw(dev, steps=20):
@@ -338,7 +346,8 @@ def decode_attention_bw(dev, steps=20):
             f"{int(lens.min())}-{int(lens.max())}, {w.H} KV heads, {Hq} query heads, d {w.D}, bf16, "
             "one layer per call", "mean_call_us": round(mean_s * 1e6, 2),
             "algorithmic_bytes_per_call": nbytes, "achieved": round(nbytes / mean_s / 1e9, 1),
-            "unit": "GB/s", "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4)}
+            "unit": "GB/s", "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4),
+            "traffic": load_traffic("decode_attention", "decode")}
 
 
 def roofline(w, rebind_ms, traffic):
@@ -439,7 +448,7 @@ def main():
         "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f64", "data": "synthetic",
         "config": describe(w),
-        "roofline": roofline(w, rebind_ms, load_counters(w, khash)),
+        "roofline": roofline(w, rebind_ms, load_traffic(f"rebind_workload{w.cfg}", "rebind")),
         "reassign_mean_us": round(sum(reassign_ms) / len(reassign_ms) * 1e3, 2),
         "kernel_source_hash": khash,
     }
@@ -452,7 +461,7 @@ def main():
         out["secondary"] = {"config": describe(w2),
                             "value": round(w2.entries() * args.steps / (t2 / 1e3), 1),
                             "unit": "entries/s", "ms_per_step": round(t2 / args.steps, 4),
-                            "roofline": roofline(w2, r2, load_counters(w2, khash))}
+                            "roofline": roofline(w2, r2, load_traffic(f"rebind_workload{w2.cfg}", "rebind"))}
         out["secondary"]["roofline"]["frac_of_copy"] = round(
             out["secondary"]["roofline"]["achieved"] / copy["achieved"], 4)
     if not args.no_small_k:

@@ -1,0 +1,151 @@
+"""Full-size parity of prefill capture and decode attention, in the shapes and
+launch configuration that bench.py times.
+
+Prefill capture (Eq. (4), (6)-(7)): 32 prompts x 2560 tokens (2048 visual, a
+64 x 32 grid), 36 layers x 8 KV heads, d 128, bf16, interleaved M-RoPE
+[22, 21, 21], one layer per call.
+* over every row on the device: cache values equal the raw values bit for bit,
+  memory rows of visual tokens equal the raw rows, the coordinates equal the
+  prompt's position ids, every rotated key pair keeps its norm within bf16 rounding;
+* a random sample of (token, head) key rows against the oracle's rotation of the
+  raw row at the token's position ids (within 1 bf16 ulp);
+* rows of other layers and slots past each prompt are unchanged (sampled).
+
+Decode attention (Eq. (14)): the active cache of the 32-sequence workload after
+its revisit (lengths 2801-4246), 8 KV heads, 32 query heads, d 128, bf16, on the
+first and the last layer; sampled (sequence, query head) outputs against the
+oracle, with the tolerance of the small-size tests.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_26631_amd as prcr
+import workloads
+from gpu_util import DEV, bf16_key, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _i16(t):
+    return t.view(torch.int16)
+
+
+def test_prefill_capture_full_size():
+    B, NL, H, D, layer = 32, 36, 8, 128, 17
+    pos, vis, n_tok, n_vis = workloads.prompt(B, n_before=(256,) * B, grid=((64, 32),) * B,
+                                              n_after=(256,) * B, frames=(1,) * B)
+    S, M = pos.shape[1], int(n_vis.max())
+    _say(f"prefill capture full size: {B} x {S} tokens, layer {layer}")
+    g = torch.Generator(device=DEV)
+    g.manual_seed(3000)
+    raw_k = torch.randn((B, S, H, D), generator=g, device=DEV).to(torch.bfloat16)
+    raw_v = torch.randn((B, S, H, D), generator=g, device=DEV).to(torch.bfloat16)
+    mem = prcr.Memory(torch.randn((B, M, NL, H, D), generator=g, device=DEV).to(torch.bfloat16),
+                      torch.randn((B, M, NL, H, D), generator=g, device=DEV).to(torch.bfloat16),
+                      torch.full((B, M, 3), -7, dtype=torch.int32, device=DEV), to_dev(n_vis))
+    s_max = S + 256
+    cache = prcr.Cache(torch.randn((B, NL, H, s_max, D), generator=g, device=DEV).to(torch.bfloat16),
+                       torch.randn((B, NL, H, s_max, D), generator=g, device=DEV).to(torch.bfloat16))
+    rope = prcr.Rope(D, (22, 21, 21), True, 5e6)
+    rng = np.random.default_rng(3001)
+    n_s = 3000
+    # untouched samples: another layer anywhere, or this layer past the prompt
+    ub, uh = rng.integers(0, B, n_s), rng.integers(0, H, n_s)
+    ul = (layer + rng.integers(1, NL, n_s)) % NL
+    us = rng.integers(0, s_max, n_s)
+    half = n_s // 2
+    ul[:half] = layer
+    us[:half] = S + rng.integers(0, s_max - S, half)
+    gt = lambda a: torch.from_numpy(np.asarray(a, np.int64)).to(DEV)
+    uidx = (gt(ub), gt(ul), gt(uh), gt(us))
+    before_k, before_v = cache.k[uidx].clone(), cache.v[uidx].clone()
+    mem_other = (gt(rng.integers(0, B, n_s)), gt(rng.integers(0, M, n_s)),
+                 gt((layer + rng.integers(1, NL, n_s)) % NL))
+    mem_before = mem.k[mem_other].clone()
+
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    start = torch.zeros(B, dtype=torch.int32, device=DEV)
+    prcr.prefill_capture(rope, mem, layer, raw_k, raw_v, to_dev(pos), to_dev(n_tok), to_dev(vis),
+                         cache, start, True, err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    assert (n_tok == S).all()
+
+    # every row: values, memory rows, coordinates, key norms
+    ck, cv = cache.k[:, layer].transpose(1, 2), cache.v[:, layer].transpose(1, 2)   # [B][s][H][D]
+    assert torch.equal(_i16(cv[:, :S]), _i16(raw_v)), "a cache value row differs from its raw row"
+    vis_t = to_dev(vis).long()
+    bb, ss = torch.nonzero(vis_t >= 0, as_tuple=True)
+    mm = vis_t[bb, ss]
+    assert torch.equal(_i16(mem.k[bb, mm, layer]), _i16(raw_k[bb, ss])), "a memory key row differs"
+    assert torch.equal(_i16(mem.v[bb, mm, layer]), _i16(raw_v[bb, ss])), "a memory value row differs"
+    assert torch.equal(mem.coords[bb, mm], to_dev(pos)[bb, ss]), "memory coordinates differ"
+    P = D // 2
+    for b0 in range(0, B, 4):
+        x = raw_k[b0:b0 + 4].float()
+        y = ck[b0:b0 + 4, :S].float()
+        nx = x[..., :P] ** 2 + x[..., P:] ** 2
+        ny = y[..., :P] ** 2 + y[..., P:] ** 2
+        assert bool(((ny - nx).abs() <= 2.0 ** -6 * nx + 1e-30).all()), "a key pair changed norm"
+
+    # sampled key rows against the oracle
+    sb, ss_, sh = rng.integers(0, B, n_s), rng.integers(0, S, n_s), rng.integers(0, H, n_s)
+    got = workloads.as_numpy_storage(ck[gt(sb), gt(ss_), gt(sh)])
+    raw = workloads.as_numpy_storage(raw_k[gt(sb), gt(ss_), gt(sh)])
+    rope_d = {"head_dim": D, "sections": (22, 21, 21), "interleaved": True, "theta": 5e6}
+    ref = oracle.rebind_row(rope_d, raw, "bf16", pos[sb, ss_].astype(np.float64))
+    d = np.abs(bf16_key(got) - bf16_key(ref))
+    assert d.max() <= 1, f"{int((d > 1).sum())} sampled key elements beyond 1 bf16 ulp"
+    _say(f"sampled keys: {int((d == 0).sum())}/{d.size} elements bit-exact")
+
+    assert torch.equal(_i16(cache.k[uidx]), _i16(before_k)), "a key row outside the prompt changed"
+    assert torch.equal(_i16(cache.v[uidx]), _i16(before_v)), "a value row outside the prompt changed"
+    assert torch.equal(_i16(mem.k[mem_other]), _i16(mem_before)), "another layer's memory changed"
+
+
+@pytest.mark.parametrize("layer", [0, 35])
+def test_decode_attention_full_size(layer):
+    w = workloads.make(3, "full")
+    Hq = 4 * w.H
+    _say(f"decode attention full size: {w.B} sequences, {w.H} KV heads, {Hq} query heads, "
+         f"layer {layer}")
+    g = torch.Generator(device=DEV)
+    g.manual_seed(4000 + layer)
+    shape = (w.B, w.NL, w.H, w.s_max, w.D)
+    cache = prcr.Cache(torch.randn(shape, generator=g, device=DEV).to(torch.bfloat16),
+                       torch.randn(shape, generator=g, device=DEV).to(torch.bfloat16))
+    rope = prcr.Rope(w.D, w.sections, w.interleaved, w.theta)
+    lens = (w.cache_len + np.diff(w.sel_off)).astype(np.int32)
+    q = torch.randn((w.B, Hq, w.D), generator=g, device=DEV).to(torch.bfloat16)
+    q_pos = (w.p_txt + 1).astype(np.int32)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out = prcr.decode_attention(rope, cache, layer, q, to_dev(q_pos), to_dev(lens), err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    out = out.cpu().numpy()
+    q_np = workloads.as_numpy_storage(q)
+    rope_d = {"head_dim": w.D, "sections": w.sections, "interleaved": w.interleaved,
+              "theta": w.theta}
+    rng = np.random.default_rng(4100 + layer)
+    G = Hq // w.H
+    worst = 0.0
+    for b in range(w.B):
+        n = int(lens[b])
+        for qh in rng.choice(Hq, 3, replace=False):
+            kvh = int(qh) // G
+            k = workloads.as_numpy_storage(cache.k[b, layer, kvh, :n])
+            v = workloads.as_numpy_storage(cache.v[b, layer, kvh, :n])
+            one = {"paged": False, "s_max": n, "k": k[None, None, None], "v": v[None, None, None]}
+            ref = oracle.decode_attention(rope_d, one, 0, q_np[b:b + 1, qh:qh + 1], q_pos[b:b + 1],
+                                          np.array([n]), w.D ** -0.5, "bf16")[0, 0]
+            vmax = np.abs(oracle.storage_to_f64(v, "bf16")).max()
+            dmax = np.abs(out[b, qh] - ref).max()
+            worst = max(worst, dmax / vmax)
+            assert dmax <= 5e-5 * vmax + 1e-6, (b, int(qh), dmax, vmax)
+    _say(f"decode attention: worst |out - ref| / max|V| = {worst:.2e}")
