@@ -302,7 +302,7 @@ prcr_status prcr_prefill_capture(const prcr_rope *rope, const prcr_mem *mem, int
 }
 
 static prcr_status decode_shape(const prcr_cache *cache, int32_t batch, int32_t n_q_heads,
-                               int32_t n_kv_heads, int32_t head_dim, int *chunk, int *n_split) {
+                               int32_t n_kv_heads, int32_t head_dim, int *n_split) {
   if (cache == nullptr) return PRCR_ERR_NULL;
   if (batch < 1 || batch > 65535 || n_kv_heads < 1 || n_kv_heads > 65535 || n_q_heads < 1 ||
       n_q_heads % n_kv_heads != 0 || n_q_heads / n_kv_heads > 8 || n_q_heads > 65535)
@@ -318,18 +318,15 @@ static prcr_status decode_shape(const prcr_cache *cache, int32_t batch, int32_t 
     cap = cache->s_max;
   }
   if (cap > INT32_MAX) return PRCR_ERR_SHAPE;
-  *chunk = decode_chunk(cap, batch, n_kv_heads);
-  const int64_t ns = (cap + *chunk - 1) / *chunk;
-  if (ns > INT32_MAX) return PRCR_ERR_SHAPE;
-  *n_split = static_cast<int>(ns);
+  *n_split = decode_splits(cap, batch, n_kv_heads);
   return PRCR_OK;
 }
 
 prcr_status prcr_decode_workspace_size(const prcr_cache *cache, int32_t batch, int32_t n_q_heads,
                                        int32_t n_kv_heads, int32_t head_dim, size_t *bytes) {
   if (bytes == nullptr) return PRCR_ERR_NULL;
-  int chunk = 0, n_split = 0;
-  const prcr_status st = decode_shape(cache, batch, n_q_heads, n_kv_heads, head_dim, &chunk, &n_split);
+  int n_split = 0;
+  const prcr_status st = decode_shape(cache, batch, n_q_heads, n_kv_heads, head_dim, &n_split);
   if (st != PRCR_OK) return st;
   *bytes = static_cast<size_t>(batch) * n_q_heads * n_split * (head_dim + 2) * sizeof(float);
   return PRCR_OK;
@@ -344,8 +341,8 @@ prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache
   prcr_status st = check_rope(rope);
   if (st != PRCR_OK) return st;
   if (dtype != PRCR_F32 && dtype != PRCR_BF16) return PRCR_ERR_DTYPE;
-  int chunk = 0, n_split = 0;
-  st = decode_shape(cache, batch, n_q_heads, n_kv_heads, rope->head_dim, &chunk, &n_split);
+  int n_split = 0;
+  st = decode_shape(cache, batch, n_q_heads, n_kv_heads, rope->head_dim, &n_split);
   if (st != PRCR_OK) return st;
   if (cache->k == nullptr || cache->v == nullptr || q == nullptr || q_pos == nullptr ||
       cache_len == nullptr || out == nullptr || workspace == nullptr ||
@@ -377,7 +374,6 @@ prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache
   p.block_size = cache->block_size;
   p.max_blocks = cache->max_blocks;
   p.n_blocks = cache->n_blocks;
-  p.chunk = chunk;
   p.n_split = n_split;
   p.scale = scale;
   for (int i = 0; i < rope->head_dim / 2; ++i)

@@ -7,9 +7,12 @@
 // Split-K flash decoding.  Kernel 1: one workgroup per (key chunk, KV head,
 // sequence) streams its keys and values once for all G query heads of the
 // group: a 16-byte chunk of a key row per lane, scores reduced across the lanes
-// of a row with shuffles, online softmax in float32.  The workgroup's key groups
-// are merged in LDS and one (max, sum, weighted V) partial per query head and
-// chunk is written to the caller's workspace.  Kernel 2 merges the chunks.
+// of a row with DPP lane permutations, online softmax in float32 with one
+// rescale per batch of rows, and only when a running maximum rose.  The
+// sequence's keys are split evenly over its workgroups.  The workgroup's key
+// groups are merged in LDS and one (max, sum, weighted V) partial per query
+// head and chunk is written to the caller's workspace.  Kernel 2 merges the
+// chunks.
 #include <cfloat>
 #include <climits>
 #include <cmath>
@@ -21,12 +24,15 @@ namespace prcr {
 namespace {
 
 #ifndef PRCR_DEC_ITERS
-#define PRCR_DEC_ITERS 1
+#define PRCR_DEC_ITERS 2
 #endif
 #ifndef PRCR_DEC_WORKGROUPS
 #define PRCR_DEC_WORKGROUPS 1024
 #endif
-constexpr int kWaves = 4;
+#ifndef PRCR_DEC_WAVES
+#define PRCR_DEC_WAVES 4
+#endif
+constexpr int kWaves = PRCR_DEC_WAVES;
 constexpr int kIters = PRCR_DEC_ITERS;   // key rows per lane group in flight
 
 template <typename T>
@@ -50,6 +56,30 @@ struct Elems<uint16_t> {
     }
   }
 };
+
+// Scores are kept in base-2 units (the query carries log2(e)), so every
+// softmax weight is one hardware exp2.
+constexpr double kLog2e = 1.4426950408889634;
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Lane permutation within a 16-lane DPP row (no LDS round trip).
+template <int kCtrl>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kCtrl, 0xF, 0xF, false));
+}
+
+// Sum over the LPK consecutive lanes that hold one key row.  Every lane of the
+// group ends with the same total: partners add the same two values at each step.
+template <int LPK>
+__device__ __forceinline__ float group_sum(float s) {
+  static_assert(LPK == 8 || LPK == 16 || LPK == 32, "unsupported lane group");
+  s += dpp<0xB1>(s);                               // quad permutation 1,0,3,2: lane ^ 1
+  s += dpp<0x4E>(s);                               // quad permutation 2,3,0,1: lane ^ 2
+  s += dpp<0x141>(s);                              // mirror in 8-lane halves: the other quad
+  if constexpr (LPK >= 16) s += dpp<0x140>(s);     // mirror in the 16-lane row: the other half
+  if constexpr (LPK >= 32) s += __shfl_xor(s, 16);
+  return s;
+}
 
 template <typename T, int D, int GT, bool kPaged>
 __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const DecodeParams p) {
@@ -79,8 +109,12 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
       atomicOr(p.err, PRCR_DERR_CAPACITY);
     len = static_cast<int>(min(max(static_cast<int64_t>(len), int64_t{0}), cap));
   }
-  const int j0 = split * p.chunk;
-  const int j1 = min(len, j0 + p.chunk);
+  // The sequence's keys are shared evenly by its n_split workgroups, in whole
+  // workgroup batches, so that no workgroup of a sequence waits on a longer one.
+  const int per = (len + p.n_split - 1) / p.n_split;
+  const int chunk = (per + KPB - 1) / KPB * KPB;
+  const int j0 = min(len, split * chunk);
+  const int j1 = min(len, j0 + chunk);
 
   // Rotated, scaled query chunk of every head of the group: the lane's elements
   // e = c*EPL .. c*EPL+EPL-1 pair with e +/- D/2, which sits in chunk c +/- LPK/2.
@@ -106,7 +140,7 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
       for (int e = 0; e < EPL; ++e) {
         const double y = first ? static_cast<double>(x[e]) * cs[e] - static_cast<double>(xp[e]) * sn[e]
                                : static_cast<double>(x[e]) * cs[e] + static_cast<double>(xp[e]) * sn[e];
-        qv[g][e] = static_cast<float>(y * p.scale);
+        qv[g][e] = static_cast<float>(y * (p.scale * kLog2e));
       }
     }
   }
@@ -132,6 +166,10 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
     for (int u = 0; u < kIters; ++u) {
       const int j = jb + u * KPB + grp;
       lv[u] = j < j1;
+      // Rows past the chunk stay zero: the update below is branch-free and a
+      // zero weight times a stale register could otherwise make a NaN.
+      kd[u] = u32x4{0u, 0u, 0u, 0u};
+      vd[u] = u32x4{0u, 0u, 0u, 0u};
       if (lv[u]) {
         int64_t row;
         if constexpr (kPaged) {
@@ -156,27 +194,44 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
     u32x4 nk[kIters], nv[kIters];
     bool nl[kIters];
     load_batch(jb + KPB * kIters, nk, nv, nl);
+    // Scores of the batch's rows for every head of the group, then one rescale
+    // of the running sums per head and batch.
+    float sc[kIters][GT];
 #pragma unroll
     for (int u = 0; u < kIters; ++u) {
-      float k[EPL], v[EPL];
+      float k[EPL];
       Elems<T>::unpack(kc[u], k);
-      Elems<T>::unpack(vc[u], v);
 #pragma unroll
       for (int g = 0; g < GT; ++g) {
         float s = 0.f;
 #pragma unroll
         for (int e = 0; e < EPL; ++e) s = fmaf(qv[g][e], k[e], s);
+        sc[u][g] = group_sum<LPK>(s);
+      }
+    }
+    float v[kIters][EPL];
 #pragma unroll
-        for (int off = LPK / 2; off > 0; off >>= 1) s += __shfl_xor(s, off);
-        if (live[u] && g < G) {
-          const float mn = fmaxf(m[g], s);
-          const float corr = __expf(m[g] - mn);
-          const float pj = __expf(s - mn);
-          l[g] = l[g] * corr + pj;
+    for (int u = 0; u < kIters; ++u) Elems<T>::unpack(vc[u], v[u]);
 #pragma unroll
-          for (int e = 0; e < EPL; ++e) o[g][e] = o[g][e] * corr + pj * v[e];
-          m[g] = mn;
-        }
+    for (int g = 0; g < GT; ++g) {
+      float mn = m[g];
+#pragma unroll
+      for (int u = 0; u < kIters; ++u) mn = live[u] ? fmaxf(mn, sc[u][g]) : mn;
+      // Rescale only when some lane's running maximum rose (rarely, after the
+      // first rows): for every other lane the factor is exactly 1.
+      if (__any(mn > m[g])) {
+        const float corr = exp2_fast(m[g] - mn);
+        l[g] *= corr;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) o[g][e] *= corr;
+        m[g] = mn;
+      }
+#pragma unroll
+      for (int u = 0; u < kIters; ++u) {
+        const float pj = live[u] ? exp2_fast(sc[u][g] - mn) : 0.f;
+        l[g] += pj;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) o[g][e] = fmaf(pj, v[u][e], o[g][e]);
       }
     }
 #pragma unroll
@@ -198,7 +253,7 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
       const float m2 = __shfl_xor(m[g], off);
       const float l2 = __shfl_xor(l[g], off);
       const float mx = fmaxf(m[g], m2);
-      const float w1 = __expf(m[g] - mx), w2 = __expf(m2 - mx);
+      const float w1 = exp2_fast(m[g] - mx), w2 = exp2_fast(m2 - mx);
       l[g] = l[g] * w1 + l2 * w2;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) o[g][e] = o[g][e] * w1 + __shfl_xor(o[g][e], off) * w2;
@@ -223,7 +278,7 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
     for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][g]);
     float Ls = 0.f, Os = 0.f;
     for (int w = 0; w < kWaves; ++w) {
-      const float wt = __expf(s_m[w][g] - M);
+      const float wt = exp2_fast(s_m[w][g] - M);
       Ls += s_l[w][g] * wt;
       Os += s_o[w][g][d] * wt;
     }
@@ -247,7 +302,7 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(const DecodeParams p)
   for (int s = 0; s < p.n_split; ++s) {
     const float l = ws[s * (D + 2) + D + 1];
     if (l > 0.f) {
-      const float w = __expf(ws[s * (D + 2) + D] - M);
+      const float w = exp2_fast(ws[s * (D + 2) + D] - M);
       Ls += l * w;
       Os += ws[s * (D + 2) + d] * w;
     }
@@ -282,13 +337,15 @@ hipError_t dispatch_dim(const DecodeParams &p, int head_dim, int G, hipStream_t 
 
 }  // namespace
 
-int decode_chunk(int64_t capacity, int batch, int n_kv_heads) {
-  // About PRCR_DEC_WORKGROUPS workgroups over the whole batch, chunks of 64..4096 keys.
-  const int64_t want = (capacity * batch * n_kv_heads + PRCR_DEC_WORKGROUPS - 1) / PRCR_DEC_WORKGROUPS;
-  int64_t chunk = (want + 63) / 64 * 64;
-  if (chunk < 64) chunk = 64;
-  if (chunk > 4096) chunk = 4096;
-  return static_cast<int>(chunk);
+int decode_splits(int64_t capacity, int batch, int n_kv_heads) {
+  // About PRCR_DEC_WORKGROUPS workgroups over the whole batch, and no split of
+  // fewer than 64 keys at full capacity.
+  const int64_t pairs = static_cast<int64_t>(batch) * n_kv_heads;
+  int64_t ns = (PRCR_DEC_WORKGROUPS + pairs - 1) / pairs;
+  const int64_t most = (capacity + 63) / 64;
+  if (ns > most) ns = most;
+  if (ns < 1) ns = 1;
+  return static_cast<int>(ns);
 }
 
 hipError_t launch_decode(const DecodeParams &p, prcr_dtype dtype, int head_dim, bool paged,

@@ -120,7 +120,7 @@ struct DecodeParams {
   int32_t *err;
   int32_t batch, n_layers, n_kv_heads, n_q_heads, layer;
   int32_t s_max, block_size, max_blocks, n_blocks;
-  int32_t chunk, n_split;
+  int32_t n_split;                // workgroups per (sequence, KV head)
   float scale;
   double inv_freq[kMaxPairs];
 };
@@ -147,6 +147,6 @@ hipError_t launch_prefill(const PrefillParams &p, prcr_dtype dtype, int head_dim
                           bool paged, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams &p, prcr_dtype dtype, int head_dim, bool paged,
                          hipStream_t stream);
-int decode_chunk(int64_t capacity, int batch, int n_kv_heads);
+int decode_splits(int64_t capacity, int batch, int n_kv_heads);
 
 }  // namespace prcr
