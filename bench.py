@@ -296,6 +296,68 @@ def prefill_capture_bw(dev, steps=20):
             "traffic": load_traffic("prefill_capture", "prefill")}
 
 
+def video_revisits(dev, reps=5):
+    """Workload 4 (8 video sequences, 28 layers x 4 KV heads, d 128, bf16): four
+    successive revisits of 1024 tokens each, 32 text tokens decoded in between
+    (cache lengths and p_txt advance on the device between revisits, untimed).
+    Each revisit is one reassign + one rebind launch, timed with HIP events on the
+    launch stream; reported per revisit and as the 4-revisit total, median over
+    reps repetitions of the whole sequence of revisits."""
+    import statistics
+
+    import numpy as np
+    import torch
+
+    import paper_2606_26631_amd as prcr
+    import workloads
+    w = workloads.make(4, "full")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    vals = workloads.torch_values(w, dev)
+    mem = prcr.Memory(vals["mem_k"], vals["mem_v"], t(w.coords), t(w.n_visual))
+    cache = prcr.Cache(vals["cache_k"], vals["cache_v"])
+    rope = prcr.Rope(w.D, w.sections, w.interleaved, w.theta)
+    sels = [(t(so), t(si), int(si.shape[0])) for so, si in w.revisits]
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    s = torch.cuda.Stream(device=dev)
+    times = [[] for _ in sels]
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        for rep in range(reps + 1):                      # the first pass is a warm-up
+            lens, p_txt = t(w.cache_len), t(w.p_txt)
+            evs = []
+            for so, si, k in sels:
+                new_pos = torch.empty((k, 3), dtype=torch.float64, device=dev)
+                next_pos = torch.empty((w.B,), dtype=torch.int32, device=dev)
+                new_len = torch.empty((w.B,), dtype=torch.int32, device=dev)
+                slots = torch.empty((k,), dtype=torch.int64, device=dev)
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(s)
+                prcr.reassign_coords(mem, so, si, p_txt, "pcr", 2, new_pos, next_pos, err, s)
+                prcr.rebind_inject(rope, mem, so, si, new_pos, cache, lens, new_len, slots, err, s)
+                b.record(s)
+                evs.append((a, b))
+                lens = new_len + w.decode_between
+                p_txt = next_pos + (w.decode_between - 1)
+            torch.cuda.synchronize()
+            if rep:
+                for r, (a, b) in enumerate(evs):
+                    times[r].append(a.elapsed_time(b))
+    if int(err.item()) != 0:
+        raise RuntimeError("device reported a data error in the video revisits")
+    entries = [k * w.NL * w.H for _, _, k in sels]
+    nbytes = [e * 4 * w.D * 2 for e in entries]
+    med = [statistics.median(x) for x in times]
+    del mem, cache, vals
+    torch.cuda.empty_cache()
+    return {"workload": f"workload 4 (video): {w.B} sequences, {w.NL} layers x {w.H} KV heads, "
+            f"d {w.D}, bf16, 4 revisits of 1024 tokens, {w.decode_between} tokens decoded between",
+            "per_revisit_us": [round(m * 1e3, 2) for m in med],
+            "per_revisit_GBs": [round(n / (m * 1e6), 1) for n, m in zip(nbytes, med)],
+            "total_us": round(sum(med) * 1e3, 2),
+            "total_entries": sum(entries), "algorithmic_bytes_total": sum(nbytes),
+            "total_GBs": round(sum(nbytes) / (sum(med) * 1e6), 1)}
+
+
 def decode_attention_bw(dev, steps=20):
     """Bandwidth of decode attention over workload 3's active cache after its revisit
     (32 sequences, lengths + 256, 36 layers x 8 KV heads, 32 query heads, d 128,
@@ -427,6 +489,7 @@ def main():
     ap.add_argument("--no-small-k", action="store_true", help="skip the small-K latency section")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-capture section")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-attention section")
+    ap.add_argument("--no-video", action="store_true", help="skip the four-revisit video section")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the rebinding path shards by sequence, KV head or "
@@ -464,6 +527,8 @@ def main():
                             "roofline": roofline(w2, r2, load_traffic(f"rebind_workload{w2.cfg}", "rebind"))}
         out["secondary"]["roofline"]["frac_of_copy"] = round(
             out["secondary"]["roofline"]["achieved"] / copy["achieved"], 4)
+    if not args.no_video:
+        out["video_revisits"] = video_revisits(dev)
     if not args.no_small_k:
         out["small_k_latency"] = small_k_latency(dev)
     if not args.no_prefill:

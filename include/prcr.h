@@ -103,14 +103,25 @@ typedef struct prcr_rope {
   double theta;
 } prcr_rope;
 
-/* Raw Visual Evidence Memory, Eq. (7). */
+/* Raw Visual Evidence Memory, Eq. (7).
+ *
+ * Key-only memory: Eq. (7) keeps both raw rows, but a value row is not rotated
+ * (Eq. (4)), so the value the prefill wrote into the standard cache is already
+ * the raw value.  With v == NULL the memory keeps keys only (half the bytes)
+ * and v_slot[b][m] names the slot of sequence b's standard cache (counted as
+ * cache_len counts slots, contiguous or paged) that holds visual token m's
+ * value rows for every layer; prcr_prefill_capture fills it.  Revisits then
+ * copy the values from that slot of the same cache, which must still hold them
+ * and must lie below cache_len[b] (else PRCR_DERR_INDEX and the token is
+ * skipped).  With v != NULL, v_slot is ignored and may be NULL. */
 typedef struct prcr_mem {
   void *k;                     /* [batch][max_visual][n_layers][n_kv_heads][head_dim] */
-  void *v;                     /* same layout                                          */
+  void *v;                     /* same layout, or NULL for a key-only memory          */
   int32_t *coords;             /* int32 [batch][max_visual][3]                          */
   const int32_t *n_visual;     /* int32 [batch], visual tokens stored per sequence     */
   int32_t batch, max_visual, n_layers, n_kv_heads, head_dim;
   prcr_dtype dtype;
+  int32_t *v_slot;             /* key-only memory: int32 [batch][max_visual]            */
 } prcr_mem;
 
 /* Active decoder cache, Eq. (13).  n_layers, n_kv_heads, head_dim and dtype are
@@ -137,6 +148,8 @@ typedef struct prcr_cache {
  * [0, s_src) is skipped with PRCR_DERR_INDEX.  mem->coords is filled by the
  * caller (it does not depend on the layer).
  */
+/* A key-only memory (mem->v == NULL) stores keys only; raw_v may then be NULL
+ * and v_slot is the caller's to fill. */
 prcr_status prcr_store_raw(const prcr_mem *mem, int32_t layer,
                            const void *raw_k, const void *raw_v, int32_t s_src,
                            const int32_t *vis_rows, int32_t *err_flag,
@@ -188,7 +201,9 @@ prcr_status prcr_reassign_coords(const prcr_mem *mem,
  * the storage type (round to nearest even); values are copied bit for bit.
  * Compiled axis maps: head_dim 64 with sections [8,12,12] or interleaved
  * [11,11,10]; head_dim 128 with [16,24,24], interleaved [22,21,21] or
- * interleaved [24,20,20]; float32 and bfloat16; contiguous and paged.
+ * interleaved [24,20,20]; float32 and bfloat16; contiguous and paged.  With a
+ * key-only memory the value rows come from cache slot v_slot[b][m] of the same
+ * sequence (see prcr_mem).
  */
 prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem,
                                const int32_t *sel_off, const int32_t *sel_idx,
@@ -216,7 +231,8 @@ prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem,
  * so rebinding a visual token at its original coordinates reproduces the key
  * written here bit for bit.  A slot beyond capacity or a bad block skips the
  * cache row (PRCR_DERR_CAPACITY / _BLOCK); m outside [0, n_visual[b]) or
- * n_tokens[b] outside [0, s_src] raise PRCR_DERR_INDEX.
+ * n_tokens[b] outside [0, s_src] raise PRCR_DERR_INDEX.  A key-only memory
+ * (mem->v == NULL) gets the raw keys and v_slot[b][m] = cache_start[b] + s.
  */
 prcr_status prcr_prefill_capture(const prcr_rope *rope, const prcr_mem *mem, int32_t layer,
                                  const void *raw_k, const void *raw_v, int32_t s_src,

@@ -272,10 +272,11 @@ def store_raw(mem_k, mem_v, layer, raw_k, raw_v, vis_rows, n_visual):
     raw_k/raw_v: [B][S_src][H][D] projections of one layer; vis_rows [B][M_max]
     gives the source row of visual token m.  Returns (mem_k, mem_v, err) as new
     arrays; rows whose source index is outside [0, S_src) are skipped with
-    ERR_INDEX.
+    ERR_INDEX.  A key-only memory (mem_v None) stores keys only: its values stay
+    in the standard cache, where Eq. (4) put them unrotated.
     """
     mem_k = np.array(mem_k, copy=True)
-    mem_v = np.array(mem_v, copy=True)
+    mem_v = None if mem_v is None else np.array(mem_v, copy=True)
     B, S_src = raw_k.shape[0], raw_k.shape[1]
     err = 0
     for b in range(B):
@@ -285,7 +286,8 @@ def store_raw(mem_k, mem_v, layer, raw_k, raw_v, vis_rows, n_visual):
                 err |= ERR_INDEX
                 continue
             mem_k[b, m, layer] = raw_k[b, r]
-            mem_v[b, m, layer] = raw_v[b, r]
+            if mem_v is not None:
+                mem_v[b, m, layer] = raw_v[b, r]
     return mem_k, mem_v, err
 
 
@@ -297,12 +299,16 @@ def prefill_capture(rope: dict, mem: dict, layer: int, raw_k, raw_v, pos, n_toke
     """One prefill layer: the standard cache gets RoPE(k_raw, p) and v_raw at slot
     cache_start[b] + s (Eq. (4)); visual rows (vis_index[b][s] = m >= 0) also go raw
     into the memory at [b][m][layer] (Eq. (6)-(7)), with their coordinates when
-    write_coords.  Returns updated copies {mem_k, mem_v, coords, k, v, err}."""
+    write_coords.  A key-only memory (mem["v"] None) keeps no values: it records in
+    mem["v_slot"][b][m] the cache slot cache_start[b] + s that holds the token's
+    value row.  Returns updated copies {mem_k, mem_v, coords, v_slot, k, v, err}."""
     dtype = mem["dtype"]
     D = rope["head_dim"]
     invf = inv_freq(rope["theta"], D)
     axis = pair_axis(D, rope["sections"], rope["interleaved"])
-    mk, mv = np.array(mem["k"], copy=True), np.array(mem["v"], copy=True)
+    mk = np.array(mem["k"], copy=True)
+    mv = None if mem["v"] is None else np.array(mem["v"], copy=True)
+    vs = None if mem.get("v_slot") is None else np.array(mem["v_slot"], copy=True)
     co = np.array(mem["coords"], copy=True)
     ck, cv = np.array(cache["k"], copy=True), np.array(cache["v"], copy=True)
     B, S = raw_k.shape[0], raw_k.shape[1]
@@ -332,10 +338,13 @@ def prefill_capture(rope: dict, mem: dict, layer: int, raw_k, raw_v, pos, n_toke
                     err |= ERR_INDEX
                     continue
                 mk[b, m, layer] = raw_k[b, s]
-                mv[b, m, layer] = raw_v[b, s]
+                if mv is not None:
+                    mv[b, m, layer] = raw_v[b, s]
+                elif vs is not None:
+                    vs[b, m] = int(cache_start[b]) + s if slot is not None else -1
                 if write_coords:
                     co[b, m] = pos[b, s]
-    return {"mem_k": mk, "mem_v": mv, "coords": co, "k": ck, "v": cv, "err": err}
+    return {"mem_k": mk, "mem_v": mv, "coords": co, "v_slot": vs, "k": ck, "v": cv, "err": err}
 
 
 # --------------------------------------------------------------------------
@@ -361,7 +370,10 @@ def rebind_inject(rope: dict, mem: dict, sel_off, sel_idx, new_pos, cache: dict,
     """Reference for one rebind-and-inject call.
 
     rope:  {"head_dim", "sections", "interleaved", "theta"}
-    mem:   {"k", "v", "n_visual", "dtype"} with k/v [B][M_max][NL][H][D]
+    mem:   {"k", "v", "n_visual", "dtype"} with k/v [B][M_max][NL][H][D].  A
+           key-only memory has v None and "v_slot" [B][M_max]: token m's value
+           rows are those of cache slot v_slot[b][m] of the same sequence, which
+           must be one of its cache_len[b] filled slots (else ERR_INDEX).
     cache: {"paged", "k", "v", "s_max" | ("block_table", "block_size",
             "max_blocks", "n_blocks")}
     Returns dict(k, v, slot_mapping, new_cache_len, err); k/v are updated copies.
@@ -387,6 +399,15 @@ def rebind_inject(rope: dict, mem: dict, sel_off, sel_idx, new_pos, cache: dict,
             if m < 0 or m >= int(mem["n_visual"][b]):
                 err |= ERR_INDEX
                 continue
+            if mem["v"] is None:
+                vsl = int(mem["v_slot"][b, m])
+                if vsl < 0 or vsl >= int(cache_len[b]):
+                    err |= ERR_INDEX
+                    continue
+                src, src_where = slot_of(cache, b, vsl)
+                if src is None:
+                    err |= src_where
+                    continue
             slot, where = slot_of(cache, b, int(cache_len[b]) + j)
             if slot is None:
                 err |= where
@@ -394,7 +415,12 @@ def rebind_inject(rope: dict, mem: dict, sel_off, sel_idx, new_pos, cache: dict,
             slot_mapping[g] = slot
             x = storage_to_f64(mem["k"][b, m], dtype)                 # [NL][H][D], Eq. (11)
             y = f64_to_storage(rotate_keys(x, new_pos[g], invf, axis), dtype)  # Eq. (12)
-            vv = mem["v"][b, m]                                       # value reuse, Eq. (12)
+            if mem["v"] is not None:                                  # value reuse, Eq. (12)
+                vv = mem["v"][b, m]
+            elif cache["paged"]:
+                vv = np.array(cache["v"][:, src_where[0], src_where[1]], copy=True)
+            else:
+                vv = np.array(cache["v"][b, :, :, src_where[1]], copy=True)
             if cache["paged"]:                                        # Eq. (13)
                 blk, off = where
                 ck[:, blk, off] = y

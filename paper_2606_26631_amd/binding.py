@@ -36,7 +36,8 @@ class CRope(ctypes.Structure):
 class CMem(ctypes.Structure):
     _fields_ = [("k", c_void_p), ("v", c_void_p), ("coords", c_void_p), ("n_visual", c_void_p),
                 ("batch", c_int32), ("max_visual", c_int32), ("n_layers", c_int32),
-                ("n_kv_heads", c_int32), ("head_dim", c_int32), ("dtype", c_int)]
+                ("n_kv_heads", c_int32), ("head_dim", c_int32), ("dtype", c_int),
+                ("v_slot", c_void_p)]
 
 
 class CCache(ctypes.Structure):
@@ -166,26 +167,37 @@ class Rope:
 
 class Memory:
     """Raw Visual Evidence Memory: k, v [B, M_max, NL, H, D]; coords [B, M_max, 3] int32;
-    n_visual [B] int32, all on one GPU."""
+    n_visual [B] int32, all on one GPU.  A key-only memory has v None and v_slot
+    [B, M_max] int32: the standard-cache slot holding visual token m's value rows."""
 
-    def __init__(self, k, v, coords, n_visual):
+    def __init__(self, k, v, coords, n_visual, v_slot=None):
         torch = _torch()
         _need(k, "mem.k", ndim=5)
-        _need(v, "mem.v", dtype=k.dtype, ndim=5, device=k.device)
-        if v.shape != k.shape:
-            raise ValueError("mem.k and mem.v shapes differ")
+        if v is None:
+            if v_slot is None:
+                raise ValueError("a key-only memory (v None) needs v_slot")
+        else:
+            _need(v, "mem.v", dtype=k.dtype, ndim=5, device=k.device)
+            if v.shape != k.shape:
+                raise ValueError("mem.k and mem.v shapes differ")
         _need(coords, "mem.coords", torch.int32, 3, k.device)
         _need(n_visual, "mem.n_visual", torch.int32, 1, k.device)
         B, M = k.shape[0], k.shape[1]
         if tuple(coords.shape) != (B, M, 3) or n_visual.shape[0] != B:
             raise ValueError("coords must be [B, M_max, 3] and n_visual [B]")
+        if v_slot is not None:
+            _need(v_slot, "mem.v_slot", torch.int32, 2, k.device)
+            if tuple(v_slot.shape) != (B, M):
+                raise ValueError("v_slot must be [B, M_max]")
         self.k, self.v, self.coords, self.n_visual = k, v, coords, n_visual
+        self.v_slot = v_slot
         self.device = k.device
 
     def to_c(self) -> CMem:
         B, M, NL, H, D = self.k.shape
-        return CMem(self.k.data_ptr(), self.v.data_ptr(), self.coords.data_ptr(),
-                    self.n_visual.data_ptr(), B, M, NL, H, D, _dtype_code(self.k))
+        return CMem(self.k.data_ptr(), None if self.v is None else self.v.data_ptr(),
+                    self.coords.data_ptr(), self.n_visual.data_ptr(), B, M, NL, H, D,
+                    _dtype_code(self.k), None if self.v_slot is None else self.v_slot.data_ptr())
 
 
 class Cache:
@@ -247,13 +259,17 @@ def _err(err, device):
 
 
 def store_raw(mem: Memory, layer: int, raw_k, raw_v, vis_rows, err=None, stream=None):
-    """Capture one layer's pre-rotary K/V rows of the visual tokens (prcr_store_raw)."""
+    """Capture one layer's pre-rotary K/V rows of the visual tokens (prcr_store_raw).
+    A key-only memory stores keys only (raw_v may be None)."""
     torch = _torch()
     B, M, NL, H, D = mem.k.shape
     _need(raw_k, "raw_k", mem.k.dtype, 4, mem.device)
-    _need(raw_v, "raw_v", mem.k.dtype, 4, mem.device)
-    if raw_k.shape != raw_v.shape or raw_k.shape[0] != B or tuple(raw_k.shape[2:]) != (H, D):
-        raise ValueError("raw_k/raw_v must be [B, S_src, H, D]")
+    if raw_k.shape[0] != B or tuple(raw_k.shape[2:]) != (H, D):
+        raise ValueError("raw_k must be [B, S_src, H, D]")
+    if mem.v is not None or raw_v is not None:
+        _need(raw_v, "raw_v", mem.k.dtype, 4, mem.device)
+        if raw_k.shape != raw_v.shape:
+            raise ValueError("raw_k/raw_v must be [B, S_src, H, D]")
     _need(vis_rows, "vis_rows", torch.int32, 2, mem.device)
     if tuple(vis_rows.shape) != (B, M):
         raise ValueError("vis_rows must be [B, M_max]")

@@ -11,7 +11,7 @@ using namespace prcr;
 
 namespace {
 
-constexpr int32_t kVersion = 1 * 10000 + 0 * 100 + 0;
+constexpr int32_t kVersion = 1 * 10000 + 1 * 100 + 0;
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -29,8 +29,9 @@ prcr_status check_rope(const prcr_rope *rope) {
 }
 
 prcr_status check_mem(const prcr_mem *mem, bool need_coords) {
-  if (mem == nullptr || mem->k == nullptr || mem->v == nullptr || mem->n_visual == nullptr)
-    return PRCR_ERR_NULL;
+  if (mem == nullptr || mem->k == nullptr || mem->n_visual == nullptr) return PRCR_ERR_NULL;
+  // A key-only memory names the cache slot of each value row instead.
+  if (mem->v == nullptr && mem->v_slot == nullptr) return PRCR_ERR_NULL;
   if (need_coords && mem->coords == nullptr) return PRCR_ERR_NULL;
   if (mem->dtype != PRCR_F32 && mem->dtype != PRCR_BF16) return PRCR_ERR_DTYPE;
   if (mem->batch < 1 || mem->max_visual < 1 || mem->n_layers < 1 || mem->n_kv_heads < 1)
@@ -42,6 +43,7 @@ prcr_status check_mem(const prcr_mem *mem, bool need_coords) {
   if (static_cast<int64_t>(mem->n_layers) * mem->n_kv_heads > INT32_MAX / 2) return PRCR_ERR_SHAPE;
   if (!aligned(mem->k, 16) || !aligned(mem->v, 16) || !aligned(mem->n_visual, 4))
     return PRCR_ERR_ALIGN;
+  if (mem->v == nullptr && !aligned(mem->v_slot, 4)) return PRCR_ERR_ALIGN;
   if (need_coords && !aligned(mem->coords, 4)) return PRCR_ERR_ALIGN;
   return PRCR_OK;
 }
@@ -101,7 +103,8 @@ prcr_status prcr_store_raw(const prcr_mem *mem, int32_t layer, const void *raw_k
                            hipStream_t stream) {
   prcr_status st = check_mem(mem, false);
   if (st != PRCR_OK) return st;
-  if (raw_k == nullptr || raw_v == nullptr || vis_rows == nullptr) return PRCR_ERR_NULL;
+  if (raw_k == nullptr || (mem->v != nullptr && raw_v == nullptr) || vis_rows == nullptr)
+    return PRCR_ERR_NULL;
   if (layer < 0 || layer >= mem->n_layers || s_src < 1 || mem->batch > 65535) return PRCR_ERR_SHAPE;
   if (!aligned(raw_k, 16) || !aligned(raw_v, 16) || !aligned(vis_rows, 4) ||
       (err_flag != nullptr && !aligned(err_flag, 4)))
@@ -111,7 +114,7 @@ prcr_status prcr_store_raw(const prcr_mem *mem, int32_t layer, const void *raw_k
   p.mem_v = mem->v;
   p.n_visual = mem->n_visual;
   p.raw_k = raw_k;
-  p.raw_v = raw_v;
+  p.raw_v = mem->v != nullptr ? raw_v : nullptr;
   p.vis_rows = vis_rows;
   p.err = err_flag;
   p.batch = mem->batch;
@@ -194,6 +197,7 @@ prcr_status prepare_rebind(const prcr_rope *rope, const prcr_mem *mem, const int
   p = RebindParams{};
   p.mem_k = mem->k;
   p.mem_v = mem->v;
+  p.v_slot = mem->v == nullptr ? mem->v_slot : nullptr;
   p.n_visual = mem->n_visual;
   p.sel_off = sel_off;
   p.sel_idx = sel_idx;
@@ -277,6 +281,7 @@ prcr_status prcr_prefill_capture(const prcr_rope *rope, const prcr_mem *mem, int
   p.vis_index = vis_index;
   p.mem_k = mem->k;
   p.mem_v = mem->v;
+  p.v_slot = mem->v == nullptr ? mem->v_slot : nullptr;
   p.coords = mem->coords;
   p.n_visual = mem->n_visual;
   p.cache_k = cache->k;

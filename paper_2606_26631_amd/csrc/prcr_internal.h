@@ -51,7 +51,8 @@ struct ReassignParams {
 
 struct RebindParams {
   const void *mem_k;
-  const void *mem_v;
+  const void *mem_v;              // null for a key-only memory
+  const int32_t *v_slot;          // key-only memory: [batch][max_visual] cache slot of the values
   const int32_t *n_visual;
   const int32_t *sel_off;
   const int32_t *sel_idx;
@@ -95,7 +96,8 @@ struct PrefillParams {
   const int32_t *n_tokens;        // [batch]
   const int32_t *vis_index;       // [batch][s_src], -1 for non-visual rows
   void *mem_k;
-  void *mem_v;
+  void *mem_v;                    // null for a key-only memory
+  int32_t *v_slot;                // key-only memory: out [batch][max_visual], or null
   int32_t *coords;
   const int32_t *n_visual;
   void *cache_k;

@@ -144,11 +144,17 @@ __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const P
         const size_t mo = (((static_cast<size_t>(b) * p.max_visual + m) * p.n_layers + p.layer) * H + h) *
                               kRowBytes + c * 16;
         char *mk = static_cast<char *>(p.mem_k) + mo;
-        char *mv = static_cast<char *>(p.mem_v) + mo;
         store_nt(mk, kl[u]);
         store_nt(mk + kHalfBytes, kh[u]);
-        store_nt(mv, vl[u]);
-        store_nt(mv + kHalfBytes, vh[u]);
+        if (p.mem_v != nullptr) {
+          char *mv = static_cast<char *>(p.mem_v) + mo;
+          store_nt(mv, vl[u]);
+          store_nt(mv + kHalfBytes, vh[u]);
+        } else if (p.v_slot != nullptr && h == 0 && c == 0) {
+          // key-only memory: the value rows stay in this cache slot (-1 if the
+          // slot could not be written)
+          p.v_slot[static_cast<int64_t>(b) * p.max_visual + m] = d >= 0 ? static_cast<int32_t>(slot) : -1;
+        }
         if (p.write_coords && h == 0 && c == 0) {
           int32_t *co = p.coords + (static_cast<int64_t>(b) * p.max_visual + m) * 3;
           co[0] = pp[0];

@@ -61,6 +61,11 @@ __device__ __forceinline__ void store16(char *p, u32x4 v) {
 // work, and afterwards always loads the next batch of rows while it stores the
 // current one.
 //
+// Key-only memory (v_slot set, no memory values): value waves copy the rows of
+// cache slot v_slot[b][m] of the same sequence, which lies below cache_len[b]
+// and so is never one of the slots this launch writes.  Their first loads wait
+// for that slot (and, paged, its block) instead of being issued early.
+//
 // kFused (the single-launch revisit): instead of reading new_pos, each key wave
 // reduces its sequence's coordinate ranges over the selection (Eq. (8)) with
 // wave shuffles and computes its own token's position (Eq. (9)-(10)); the first
@@ -130,18 +135,23 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
   }
   const int b = __builtin_amdgcn_readfirstlane(cnt - 1);
 
-  // The source rows exist whenever b and m are in range: start loading them.
+  // The source rows exist whenever b and m are in range: start loading them
+  // (memory rows; cache rows of a key-only memory are loaded after validation).
+  const bool alias_v = !keys && p.v_slot != nullptr;
   const bool src_ok = b >= 0 && b < p.batch && m >= 0 && m < p.max_visual;
   const size_t tok_off = src_ok ? (static_cast<size_t>(b) * p.max_visual + m) * rows_total : 0;
-  const char *src = static_cast<const char *>(keys ? p.mem_k : p.mem_v) + tok_off * kRowBytes + c * 16;
+  const char *src = static_cast<const char *>(keys ? p.mem_k : (alias_v ? p.cache_v : p.mem_v)) +
+                    (alias_v ? 0 : tok_off * kRowBytes) + c * 16;
   char *dst = static_cast<char *>(keys ? p.cache_k : p.cache_v) + c * 16;
   u32x4 lo[kUnroll], hi[kUnroll];
+  if (!alias_v) {
 #pragma unroll
-  for (int u = 0; u < kUnroll; ++u) {
-    const int row = row0 + u * RPI + r;
-    if (src_ok && row < row_end) {
-      lo[u] = load16(src + static_cast<size_t>(row) * kRowBytes);
-      hi[u] = load16(src + static_cast<size_t>(row) * kRowBytes + kHalfBytes);
+    for (int u = 0; u < kUnroll; ++u) {
+      const int row = row0 + u * RPI + r;
+      if (src_ok && row < row_end) {
+        lo[u] = load16(src + static_cast<size_t>(row) * kRowBytes);
+        hi[u] = load16(src + static_cast<size_t>(row) * kRowBytes + kHalfBytes);
+      }
     }
   }
 
@@ -211,6 +221,32 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
       }
     }
   }
+  // Key-only memory: the value slot must be one of the sequence's filled slots.
+  int64_t vslot = 0, vpool = 0;
+  if (ok && p.v_slot != nullptr) {
+    vslot = p.v_slot[static_cast<int64_t>(b) * p.max_visual + m];
+    if (vslot < 0 || vslot >= p.cache_len[b]) {
+      ok = false;
+      flags = PRCR_DERR_INDEX;
+    } else if constexpr (kPaged) {
+      const int64_t lb = vslot / p.block_size;
+      if (lb >= p.max_blocks) {
+        ok = false;
+        flags = PRCR_DERR_CAPACITY;
+      } else {
+        const int64_t vb = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
+        if (vb < 0 || vb >= p.n_blocks) {
+          ok = false;
+          flags = PRCR_DERR_BLOCK;
+        } else {
+          vpool = vb * p.block_size + (vslot - lb * p.block_size);
+        }
+      }
+    } else if (vslot >= p.s_max) {
+      ok = false;
+      flags = PRCR_DERR_CAPACITY;
+    }
+  }
   int64_t slot_id = -1, blk = 0, off = 0;
   if (ok) {
     if constexpr (kPaged) {
@@ -241,23 +277,35 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
   }
   if (!ok) return;
 
-  // Destination row offsets (in rows of head_dim elements).
-  size_t dst_base;
-  if constexpr (kPaged) {
-    dst_base = static_cast<size_t>(blk) * p.block_size + off;   // slot within a layer's pool
-  } else {
-    dst_base = static_cast<size_t>(b) * rows_total;             // first (layer, head) row of b
-  }
-  auto dst_offset = [&](int row) -> size_t {
+  // Destination slot within a layer's block pool (paged only).
+  const size_t dst_pool = kPaged ? static_cast<size_t>(blk) * p.block_size + off : 0;
+  // Byte offset of (layer, head) row `row` of a cache slot: `pool` is the slot
+  // within a layer's block pool (paged), `sl` the sequence's slot (contiguous).
+  auto cache_offset = [&](int row, size_t pool, int64_t sl) -> size_t {
     if constexpr (kPaged) {
       const int l = row / p.n_kv_heads;
       const int h = row - l * p.n_kv_heads;
-      return ((static_cast<size_t>(l) * p.n_blocks * p.block_size + dst_base) * p.n_kv_heads + h) *
+      return ((static_cast<size_t>(l) * p.n_blocks * p.block_size + pool) * p.n_kv_heads + h) *
              kRowBytes;
     } else {
-      return ((dst_base + row) * p.s_max + slot) * kRowBytes;
+      return ((static_cast<size_t>(b) * rows_total + row) * p.s_max + sl) * kRowBytes;
     }
   };
+  auto dst_offset = [&](int row) -> size_t { return cache_offset(row, dst_pool, slot); };
+  auto src_offset = [&](int row) -> size_t {
+    return alias_v ? cache_offset(row, static_cast<size_t>(vpool), vslot)
+                   : static_cast<size_t>(row) * kRowBytes;
+  };
+  if (alias_v) {
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int row = row0 + u * RPI + r;
+      if (row < row_end) {
+        lo[u] = load16(src + src_offset(row));
+        hi[u] = load16(src + src_offset(row) + kHalfBytes);
+      }
+    }
+  }
 
   // cos/sin of this token's angles (keys only): lane i computes pair i (mod P),
   // then lane (r, c) gathers the pairs c*E .. c*E+E-1 of its two chunks.
@@ -282,8 +330,8 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
     for (int u = 0; u < kUnroll; ++u) {
       const int row = nb + u * RPI + r;
       if (row < row_end) {
-        nlo[u] = load16(src + static_cast<size_t>(row) * kRowBytes);
-        nhi[u] = load16(src + static_cast<size_t>(row) * kRowBytes + kHalfBytes);
+        nlo[u] = load16(src + src_offset(row));
+        nhi[u] = load16(src + src_offset(row) + kHalfBytes);
       }
     }
 #pragma unroll

@@ -25,13 +25,16 @@ __global__ __launch_bounds__(kWaves * kWave) void store_raw_kernel(const StorePa
   const size_t src = (static_cast<size_t>(b) * p.s_src + r) * p.row_bytes;
   const size_t dst = ((static_cast<size_t>(b) * p.max_visual + m) * p.n_layers + p.layer) * p.row_bytes;
   const char *sk = static_cast<const char *>(p.raw_k) + src;
-  const char *sv = static_cast<const char *>(p.raw_v) + src;
   char *dk = static_cast<char *>(p.mem_k) + dst;
-  char *dv = static_cast<char *>(p.mem_v) + dst;
   for (int o = lane * 16; o < p.row_bytes; o += kWave * 16) {
     const u32x4 k = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(sk + o));
-    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(sv + o));
     __builtin_nontemporal_store(k, reinterpret_cast<u32x4 *>(dk + o));
+  }
+  if (p.mem_v == nullptr) return;   // key-only memory
+  const char *sv = static_cast<const char *>(p.raw_v) + src;
+  char *dv = static_cast<char *>(p.mem_v) + dst;
+  for (int o = lane * 16; o < p.row_bytes; o += kWave * 16) {
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(sv + o));
     __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(dv + o));
   }
 }

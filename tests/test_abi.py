@@ -29,7 +29,7 @@ def test_library_exports_every_declared_function():
     assert {"prcr_store_raw", "prcr_reassign_coords", "prcr_rebind_inject"} <= set(names)
     for n in names:
         assert hasattr(L, n), f"{n} declared in prcr.h but not exported"
-    assert L.prcr_version() == 10000
+    assert L.prcr_version() == 10100
 
 
 def test_status_strings():
@@ -128,6 +128,11 @@ def test_rebind_validation_errors():
     assert call_rebind(r2, m2, c2) == 2
     r2, m2, c2 = good(); m2.batch = 0
     assert call_rebind(r2, m2, c2) == 2
+    # key-only memory: no values needs the value-slot table, aligned
+    r2, m2, c2 = good(); m2.v = None
+    assert call_rebind(r2, m2, c2) == 1
+    r2, m2, c2 = good(); m2.v, m2.v_slot = None, FAKE + 2
+    assert call_rebind(r2, m2, c2) == 4
 
 
 def test_reassign_validation_errors():
@@ -150,6 +155,8 @@ def test_store_validation_errors():
     assert call_store(mem, s_src=0) == 2
     assert call_store(mem, raw_k=None) == 1
     assert call_store(mem, raw_k=FAKE + 8) == 4
+    m2 = good()[1]; m2.v = None
+    assert call_store(m2) == 1                         # key-only memory without v_slot
 
 
 def call_revisit(rope, mem, cache, mode=0, l_ext=2, p_txt=FAKE, next_pos=FAKE + 0x200,

@@ -1,6 +1,10 @@
 """GPU parity of the fused prefill capture (prcr_prefill_capture) against the
 oracle, and the end-to-end property that a revisit at the original coordinates
-(IDENTITY reassignment) reproduces the keys the prefill wrote, bit for bit."""
+(IDENTITY reassignment) reproduces the keys the prefill wrote, bit for bit.
+
+Also the key-only memory (values left in the standard cache, found through the
+memory's value-slot table): prefill capture, then PCR revisits (two launches and
+fused) against the oracle, and a value slot that is not yet filled."""
 import numpy as np
 import pytest
 import torch
@@ -21,7 +25,7 @@ def _say(msg):
 
 
 class Prefill:
-    def __init__(self, dtype, D, sections, inter, paged, NL=3, H=3, seed=5):
+    def __init__(self, dtype, D, sections, inter, paged, NL=3, H=3, seed=5, key_only=False):
         self.pos, self.vis_index, self.n_tokens, self.n_visual = workloads.prompt()
         B, S = self.vis_index.shape
         M = int(self.n_visual.max()) + 2
@@ -33,7 +37,8 @@ class Prefill:
         rnd = lambda *shape: torch.randn(shape, generator=g).to(tdt)
         self.raw = [(rnd(B, S, H, D), rnd(B, S, H, D)) for _ in range(NL)]
         self.mem_k = torch.zeros((B, M, NL, H, D), dtype=tdt)
-        self.mem_v = torch.zeros_like(self.mem_k)
+        self.mem_v = None if key_only else torch.zeros_like(self.mem_k)
+        self.key_only = key_only
         self.paged = paged
         if paged:
             bs = 4
@@ -56,9 +61,11 @@ class Prefill:
     def run_gpu(self, vis_index=None, start=None):
         vis = self.vis_index if vis_index is None else vis_index
         st = np.zeros(self.B, np.int32) if start is None else np.asarray(start, np.int32)
-        mem = prcr.Memory(self.mem_k.to(DEV), self.mem_v.to(DEV),
+        v_slot = (torch.full((self.B, self.M), -5, dtype=torch.int32, device=DEV)
+                  if self.key_only else None)
+        mem = prcr.Memory(self.mem_k.to(DEV), None if self.key_only else self.mem_v.to(DEV),
                           torch.zeros((self.B, self.M, 3), dtype=torch.int32, device=DEV),
-                          to_dev(self.n_visual))
+                          to_dev(self.n_visual), v_slot)
         cache = prcr.Cache(self.cache_k.to(DEV), self.cache_v.to(DEV),
                            to_dev(self.cache_cfg["block_table"]) if self.paged else None)
         rope = prcr.Rope(self.D, self.rope["sections"], self.rope["interleaved"], self.rope["theta"])
@@ -73,7 +80,9 @@ class Prefill:
         vis = self.vis_index if vis_index is None else vis_index
         st = np.zeros(self.B, np.int64) if start is None else np.asarray(start, np.int64)
         npy = workloads.as_numpy_storage
-        mem = {"k": npy(self.mem_k), "v": npy(self.mem_v), "coords": np.zeros((self.B, self.M, 3), np.int32),
+        mem = {"k": npy(self.mem_k), "v": None if self.key_only else npy(self.mem_v),
+               "v_slot": np.full((self.B, self.M), -5, np.int32) if self.key_only else None,
+               "coords": np.zeros((self.B, self.M, 3), np.int32),
                "n_visual": self.n_visual, "dtype": self.dtype}
         cache = dict(self.cache_cfg, k=npy(self.cache_k), v=npy(self.cache_v))
         err = 0
@@ -81,7 +90,7 @@ class Prefill:
             out = oracle.prefill_capture(self.rope, mem, layer, npy(rk), npy(rv), self.pos, self.n_tokens,
                                          vis, True, cache, st)
             err |= out["err"]
-            mem = dict(mem, k=out["mem_k"], v=out["mem_v"], coords=out["coords"])
+            mem = dict(mem, k=out["mem_k"], v=out["mem_v"], coords=out["coords"], v_slot=out["v_slot"])
             cache = dict(cache, k=out["k"], v=out["v"])
         return mem, cache, err
 
@@ -89,7 +98,11 @@ class Prefill:
 def _compare(pf, mem, cache, err, ref_mem, ref_cache, ref_err):
     npy = workloads.as_numpy_storage
     assert err == ref_err
-    assert np.array_equal(npy(mem.k), ref_mem["k"]) and np.array_equal(npy(mem.v), ref_mem["v"])
+    assert np.array_equal(npy(mem.k), ref_mem["k"])
+    if pf.key_only:
+        assert np.array_equal(mem.v_slot.cpu().numpy(), ref_mem["v_slot"])
+    else:
+        assert np.array_equal(npy(mem.v), ref_mem["v"])
     assert np.array_equal(mem.coords.cpu().numpy(), ref_mem["coords"])
     assert np.array_equal(npy(cache.v), ref_cache["v"])
     gk = npy(cache.k)
@@ -151,3 +164,76 @@ def test_identity_revisit_reproduces_prefill_keys(paged):
                 c = (new // pf.cache_cfg["s_max"], slice(None), slice(None), new % pf.cache_cfg["s_max"])
             assert torch.equal(cache.k[a].view(torch.int16), cache.k[c].view(torch.int16))
             assert torch.equal(cache.v[a].view(torch.int16), cache.v[c].view(torch.int16))
+
+
+# --- key-only memory ---------------------------------------------------------
+KEY_ONLY = [("bf16", 128, (24, 20, 20), True), ("f32", 64, (8, 12, 12), False)]
+
+
+@pytest.mark.parametrize("paged", [False, True])
+@pytest.mark.parametrize("dtype,D,sections,inter", KEY_ONLY)
+def test_key_only_prefill_parity(dtype, D, sections, inter, paged):
+    pf = Prefill(dtype, D, sections, inter, paged, key_only=True)
+    _say(f"key-only prefill capture {dtype} D={D} paged={paged}")
+    mem, cache, rope, err = pf.run_gpu()
+    ref_mem, ref_cache, ref_err = pf.run_oracle()
+    _compare(pf, mem, cache, err, ref_mem, ref_cache, ref_err)
+
+
+def _key_only_revisit(pf, sel_off, sel_idx, fused, v_slot_patch=None):
+    """Key-only prefill on both sides, then one PCR revisit on both; returns
+    (GPU cache, slots, new lengths, err) and the oracle's result."""
+    mem, cache, rope, err = pf.run_gpu()
+    ref_mem, ref_cache, _ = pf.run_oracle()
+    assert err == 0
+    if v_slot_patch is not None:
+        b, m, v = v_slot_patch
+        mem.v_slot[b, m] = v
+        ref_mem["v_slot"][b, m] = v
+    p_txt = (pf.n_tokens - 1).astype(np.int32)
+    err_t = torch.zeros(1, dtype=torch.int32, device=DEV)
+    so, si = to_dev(sel_off), to_dev(sel_idx)
+    if fused:
+        _, _, new_len, slots = prcr.revisit(rope, mem, so, si, to_dev(p_txt), cache,
+                                            to_dev(pf.n_tokens), "pcr", 2, err=err_t)
+    else:
+        new_pos, _ = prcr.reassign_coords(mem, so, si, to_dev(p_txt), "pcr", 2, err=err_t)
+        new_len, slots = prcr.rebind_inject(rope, mem, so, si, new_pos, cache, to_dev(pf.n_tokens),
+                                            err=err_t)
+    torch.cuda.synchronize()
+    pos_o, _, _ = oracle.reassign_batch(ref_mem["coords"], ref_mem["n_visual"], sel_off, sel_idx,
+                                        p_txt, "pcr", 2)
+    ref = oracle.rebind_inject(pf.rope, ref_mem, sel_off, sel_idx, pos_o, ref_cache, pf.n_tokens)
+    return cache, slots.cpu().numpy(), new_len.cpu().numpy(), int(err_t.item()), ref
+
+
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("paged", [False, True])
+def test_key_only_revisit_parity(paged, fused):
+    """Values of the revisited tokens come from the prompt slots the prefill wrote."""
+    pf = Prefill("bf16", 128, (16, 24, 24), False, paged, NL=4, H=4, key_only=True)
+    sel_off = np.array([0, 5, 8], np.int32)
+    sel_idx = np.array([0, 3, 7, 11, 23, 2, 5, 29], np.int32)
+    _say(f"key-only revisit paged={paged} fused={fused}")
+    cache, slots, new_len, err, ref = _key_only_revisit(pf, sel_off, sel_idx, fused)
+    npy = workloads.as_numpy_storage
+    assert err == ref["err"] == 0
+    assert np.array_equal(slots, ref["slot_mapping"])
+    assert np.array_equal(new_len, ref["new_cache_len"])
+    assert np.array_equal(npy(cache.v), ref["v"])
+    assert_keys_close(npy(cache.k), ref["k"], "bf16")
+
+
+def test_key_only_value_slot_not_filled():
+    """A value slot at or beyond cache_len is rejected: flag, token skipped."""
+    pf = Prefill("bf16", 128, (16, 24, 24), False, False, NL=2, H=2, key_only=True)
+    sel_off = np.array([0, 3, 5], np.int32)
+    sel_idx = np.array([1, 4, 9, 2, 5], np.int32)
+    patch = (0, 4, int(pf.n_tokens[0]))          # sequence 0, token 4 -> first free slot
+    _say("key-only revisit with a value slot that is not filled")
+    cache, slots, new_len, err, ref = _key_only_revisit(pf, sel_off, sel_idx, False, patch)
+    npy = workloads.as_numpy_storage
+    assert err == ref["err"] == oracle.ERR_INDEX
+    assert slots[1] == -1 and np.array_equal(slots, ref["slot_mapping"])
+    assert np.array_equal(npy(cache.v), ref["v"])
+    assert_keys_close(npy(cache.k), ref["k"], "bf16")

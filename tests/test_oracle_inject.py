@@ -108,6 +108,67 @@ def test_inject_brute_force(paged, dtype):
     assert out["err"] == 0
 
 
+def _value_rows_brute(cache, b, slot, NL, H):
+    """Value rows [NL][H] of logical slot `slot` of sequence b, by walking the
+    block table by hand (paged) or indexing the sequence's rows (contiguous)."""
+    rows = []
+    for l in range(NL):
+        for h in range(H):
+            if cache["paged"]:
+                blk = cache["block_table"][b][slot // cache["block_size"]]
+                rows.append(cache["v"][l, blk, slot % cache["block_size"], h])
+            else:
+                rows.append(cache["v"][b, l, h, slot])
+    return np.array(rows).reshape((NL, H) + rows[0].shape)
+
+
+@pytest.mark.parametrize("paged", [False, True])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_key_only_memory_takes_values_from_the_cache(paged, dtype):
+    """Key-only memory: the value rows injected for token m are those of cache slot
+    v_slot[b][m] (a filled slot of the same sequence); keys are as with a full memory."""
+    rope, mem, sel_off, sel_idx, new_pos, cache, cache_len = _tiny(paged, dtype)
+    B, M, NL, H, D = mem["k"].shape
+    v_slot = np.stack([RNG.integers(0, cache_len[b], M) for b in range(B)]).astype(np.int32)
+    konly = {"k": mem["k"], "v": None, "v_slot": v_slot, "n_visual": mem["n_visual"],
+             "dtype": dtype}
+    full = rebind_inject(rope, mem, sel_off, sel_idx, new_pos, cache, cache_len)
+    out = rebind_inject(rope, konly, sel_off, sel_idx, new_pos, cache, cache_len)
+    assert out["err"] == 0
+    assert np.array_equal(out["k"], full["k"])
+    assert out["slot_mapping"].tolist() == full["slot_mapping"].tolist()
+    ev = cache["v"].copy()
+    for b in range(B):
+        for j in range(sel_off[b + 1] - sel_off[b]):
+            m = sel_idx[sel_off[b] + j]
+            want = _value_rows_brute(cache, b, int(v_slot[b, m]), NL, H)
+            s = cache_len[b] + j
+            for l in range(NL):
+                for h in range(H):
+                    if paged:
+                        blk = cache["block_table"][b][s // cache["block_size"]]
+                        ev[l, blk, s % cache["block_size"], h] = want[l, h]
+                    else:
+                        ev[b, l, h, s] = want[l, h]
+    assert np.array_equal(out["v"], ev)
+
+
+def test_key_only_memory_value_slot_must_be_filled():
+    rope, mem, sel_off, sel_idx, new_pos, cache, cache_len = _tiny(False)
+    B, M = mem["k"].shape[:2]
+    v_slot = np.zeros((B, M), np.int32)
+    v_slot[0, 4] = cache_len[0]          # token 4 of sequence 0 (first pick): not yet filled
+    v_slot[2, 3] = -1                    # token 3 of sequence 2 (last pick)
+    konly = {"k": mem["k"], "v": None, "v_slot": v_slot, "n_visual": mem["n_visual"],
+             "dtype": "f32"}
+    out = rebind_inject(rope, konly, sel_off, sel_idx, new_pos, cache, cache_len)
+    assert out["err"] == ERR_INDEX
+    assert out["slot_mapping"][0] == -1 and out["slot_mapping"][6] == -1
+    assert (out["slot_mapping"][1:6] >= 0).all()
+    assert np.array_equal(out["k"][0, :, :, cache_len[0]], cache["k"][0, :, :, cache_len[0]])
+    assert np.array_equal(out["v"][2, :, :, cache_len[2] + 3], cache["v"][2, :, :, cache_len[2] + 3])
+
+
 def test_paged_concat_through_block_table():
     """Eq. (13): the logical sequence read through the block table is Concat[old, new]."""
     rope, mem, sel_off, sel_idx, new_pos, cache, cache_len = _tiny(True)

@@ -50,7 +50,7 @@ def _capture_all(rope, mem, cache, raw, pos, vis_index, n_tokens):
         out = oracle.prefill_capture(rope, mem, layer, rk, rv, pos, n_tokens, vis_index, True, cache,
                                      start)
         assert out["err"] == 0
-        mem = dict(mem, k=out["mem_k"], v=out["mem_v"], coords=out["coords"])
+        mem = dict(mem, k=out["mem_k"], v=out["mem_v"], coords=out["coords"], v_slot=out["v_slot"])
         cache = dict(cache, k=out["k"], v=out["v"])
     return mem, cache
 
@@ -117,6 +117,44 @@ def test_identity_rebinding_reproduces_prefill_keys():
                 else:
                     a, c = out["k"][b, :, :, s_orig], out["k"][b, :, :, s_new]
                 assert np.array_equal(a, c)
+
+
+def test_key_only_memory_prefill_and_identity_round_trip():
+    """A key-only memory gets the same keys and, per visual token, the prompt slot
+    that holds its value rows; an IDENTITY revisit through it then reproduces the
+    prefill's key and value rows at the new slots (values read from the cache)."""
+    for paged in (False, True):
+        rope, mem, cache, raw, pos, vis_index, n_tokens = _setup(paged=paged)
+        full, cache_f = _capture_all(rope, mem, cache, raw, pos, vis_index, n_tokens)
+        konly = dict(mem, v=None, v_slot=np.full(mem["coords"].shape[:2], -5, np.int32))
+        konly, cache_k = _capture_all(rope, konly, cache, raw, pos, vis_index, n_tokens)
+        assert konly["v"] is None
+        assert np.array_equal(konly["k"], full["k"]) and np.array_equal(cache_k["k"], cache_f["k"])
+        for b in range(2):
+            for s_ in range(int(n_tokens[b])):
+                m = vis_index[b, s_]
+                if m >= 0:
+                    assert konly["v_slot"][b, m] == s_
+        assert (konly["v_slot"][0, int(full["n_visual"][0]):] == -5).all()
+        sel = [np.array([0, 3, 7, 11]), np.array([2, 5, 29])]
+        sel_off = np.array([0, 4, 7])
+        sel_idx = np.concatenate(sel)
+        new_pos, _, err = oracle.reassign_batch(konly["coords"], konly["n_visual"], sel_off, sel_idx,
+                                                n_tokens - 1, "identity")
+        out = oracle.rebind_inject(rope, konly, sel_off, sel_idx, new_pos, cache_k, n_tokens)
+        assert err == 0 and out["err"] == 0
+        for b in range(2):
+            for j, m in enumerate(sel[b]):
+                s_orig = int(np.nonzero(vis_index[b] == m)[0][0])
+                s_new = int(n_tokens[b]) + j
+                for which in ("k", "v"):
+                    if paged:
+                        bs, t = cache["block_size"], cache["block_table"]
+                        a = out[which][:, t[b][s_orig // bs], s_orig % bs]
+                        c = out[which][:, t[b][s_new // bs], s_new % bs]
+                    else:
+                        a, c = out[which][b, :, :, s_orig], out[which][b, :, :, s_new]
+                    assert np.array_equal(a, c)
 
 
 def test_prefill_errors():
