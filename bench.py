@@ -77,7 +77,7 @@ def load_traffic(name: str, kind: str):
 
 
 class Prepared:
-    def __init__(self, w, dev):
+    def __init__(self, w, dev, key_only=False):
         import numpy as np
         import torch
 
@@ -86,7 +86,12 @@ class Prepared:
         t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
         self.w = w
         vals = workloads.torch_values(w, dev)
-        self.mem = prcr.Memory(vals["mem_k"], vals["mem_v"], t(w.coords), t(w.n_visual))
+        if key_only:
+            del vals["mem_v"]
+            self.mem = prcr.Memory(vals["mem_k"], None, t(w.coords), t(w.n_visual),
+                                   t(workloads.value_slots(w)))
+        else:
+            self.mem = prcr.Memory(vals["mem_k"], vals["mem_v"], t(w.coords), t(w.n_visual))
         self.cache = prcr.Cache(vals["cache_k"], vals["cache_v"], t(w.block_table) if w.paged else None)
         self.rope = prcr.Rope(w.D, w.sections, w.interleaved, w.theta)
         self.sel_off, self.sel_idx = t(w.sel_off), t(w.sel_idx)
@@ -108,9 +113,9 @@ class Prepared:
                            self.cache, self.cache_len, self.new_len, self.slots, self.err, stream)
 
 
-def measure(w, steps, warmup, dev):
+def measure(w, steps, warmup, dev, key_only=False):
     import torch
-    p = Prepared(w, dev)
+    p = Prepared(w, dev, key_only)
     s = torch.cuda.Stream(device=dev)
     torch.cuda.synchronize()
     with torch.cuda.stream(s):
@@ -490,6 +495,7 @@ def main():
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-capture section")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-attention section")
     ap.add_argument("--no-video", action="store_true", help="skip the four-revisit video section")
+    ap.add_argument("--no-key-only", action="store_true", help="skip the key-only memory section")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the rebinding path shards by sequence, KV head or "
@@ -527,6 +533,13 @@ def main():
                             "roofline": roofline(w2, r2, load_traffic(f"rebind_workload{w2.cfg}", "rebind"))}
         out["secondary"]["roofline"]["frac_of_copy"] = round(
             out["secondary"]["roofline"]["achieved"] / copy["achieved"], 4)
+    if not args.no_key_only:
+        wk = workloads.make(args.workload, "full")
+        _, rk, _ = measure(wk, args.steps, args.warmup, dev, key_only=True)
+        out["key_only_memory"] = {
+            "workload": f"workload {wk.cfg} ({wk.name}), key-only memory: values copied from "
+                        "the prompt slots of the same cache",
+            "roofline": roofline(wk, rk, None)}
     if not args.no_video:
         out["video_revisits"] = video_revisits(dev)
     if not args.no_small_k:

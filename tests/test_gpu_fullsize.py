@@ -11,6 +11,9 @@ Workloads 3 (32 sequences, contiguous), 4 (video, four successive revisits) and 
   equals its memory row bit for bit, and each rotated key pair keeps its norm within
   bf16 rounding;
 * a random sample of cache rows outside the new slots is unchanged.
+
+The key-only memory runs at workloads 3 and 5 too: every injected value row equals
+the cache row at the token's value slot, keys as above.
 """
 import numpy as np
 import pytest
@@ -58,8 +61,9 @@ def _untouched_sample(w, new_slots, rng, n=N_SAMPLE):
     return tuple(torch.tensor(np.array(c), device=DEV) for c in zip(*picks))
 
 
-def _check_call(w, mem, cache, rope, sel_off, sel_idx, p_txt, cache_len, rng):
-    """One reassign + rebind call at full size, checked as described above."""
+def _check_call(w, mem, cache, rope, sel_off, sel_idx, p_txt, cache_len, rng, v_slot=None):
+    """One reassign + rebind call at full size, checked as described above.  With
+    v_slot (a key-only memory) the values come from those cache slots."""
     B = w.B
     oc = _oracle_cache(w)
     exp_slots = np.full(len(sel_idx), -1, np.int64)
@@ -91,9 +95,16 @@ def _check_call(w, mem, cache, rope, sel_off, sel_idx, p_txt, cache_len, rng):
     tok_m = si.long()
     sl = slots
     got_v = _rows_at(w, cache.v, sl)
-    assert torch.equal(got_v.view(torch.int16), mem.v[tok_b, tok_m].view(torch.int16)), \
-        "a value row differs from its memory row"
-    del got_v
+    if v_slot is None:
+        want_v = mem.v[tok_b, tok_m]
+    else:
+        tb = np.repeat(np.arange(B), np.diff(sel_off))
+        src = np.array([oracle.slot_of(oc, int(b), int(v_slot[b, m]))[0]
+                        for b, m in zip(tb, sel_idx)], np.int64)
+        want_v = _rows_at(w, cache.v, torch.from_numpy(src).to(DEV))
+    assert torch.equal(got_v.view(torch.int16), want_v.view(torch.int16)), \
+        "a value row differs from its source row"
+    del got_v, want_v
     P = w.D // 2
     for t0 in range(0, len(sel_idx), 2048):
         t1 = min(len(sel_idx), t0 + 2048)
@@ -111,7 +122,6 @@ def _check_call(w, mem, cache, rope, sel_off, sel_idx, p_txt, cache_len, rng):
     m = sel_idx[g]
     gt = lambda a: torch.from_numpy(np.asarray(a, np.int64)).to(DEV)
     raw_k = workloads.as_numpy_storage(mem.k[gt(b), gt(m), gt(l), gt(h)])
-    raw_v = workloads.as_numpy_storage(mem.v[gt(b), gt(m), gt(l), gt(h)])
     sid = exp_slots[g]
     if w.paged:
         idx = (gt(l), gt(sid // w.block_size), gt(sid % w.block_size), gt(h))
@@ -122,7 +132,8 @@ def _check_call(w, mem, cache, rope, sel_off, sel_idx, p_txt, cache_len, rng):
     ref_k = oracle.rebind_row(w.rope(), raw_k, w.dtype, pos_o[g])
     d = np.abs(bf16_key(got_k) - bf16_key(ref_k))
     assert d.max() <= 1, f"{int((d > 1).sum())} sampled key elements beyond 1 bf16 ulp"
-    assert np.array_equal(got_v, raw_v)
+    if v_slot is None:
+        assert np.array_equal(got_v, workloads.as_numpy_storage(mem.v[gt(b), gt(m), gt(l), gt(h)]))
 
     # rows outside the new slots are unchanged
     assert torch.equal(cache.k[untouched].view(torch.int16), before_k.view(torch.int16)), \
@@ -167,4 +178,22 @@ def test_full_size_video_four_revisits():
         p_txt = nxt + w.decode_between - 1
     assert (lens <= w.s_max).all()
     del mem, cache
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("cfg", [3, 5])
+def test_full_size_key_only_memory(cfg):
+    w = workloads.make(cfg, "full")
+    _say(f"workload {cfg} full, key-only memory")
+    vals = workloads.torch_values(w, DEV)
+    del vals["mem_v"]
+    v_slot = workloads.value_slots(w)
+    mem = prcr.Memory(vals["mem_k"], None, to_dev(w.coords), to_dev(w.n_visual), to_dev(v_slot))
+    cache = prcr.Cache(vals["cache_k"], vals["cache_v"], to_dev(w.block_table) if w.paged else None)
+    rope = prcr.Rope(w.D, w.sections, w.interleaved, w.theta)
+    rng = np.random.default_rng(cfg + 50)
+    exact, n, _, _ = _check_call(w, mem, cache, rope, w.sel_off, w.sel_idx, w.p_txt.astype(np.int64),
+                                 w.cache_len.astype(np.int64), rng, v_slot=v_slot)
+    _say(f"  sampled keys bit-exact {exact}/{n}")
+    del mem, cache, vals
     torch.cuda.empty_cache()

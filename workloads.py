@@ -218,6 +218,21 @@ def make(cfg: int, scale: str = "full", seed: int | None = None) -> Workload:
 # --------------------------------------------------------------------------
 # Tensor contents
 # --------------------------------------------------------------------------
+def value_slots(w: Workload) -> np.ndarray:
+    """Value-slot table of a key-only memory for workload w, int32 [B][M_max]: the
+    prompt is read as up to 64 text tokens followed by the visual tokens, so visual
+    token m of sequence b sits at slot prefix + m, below the sequence's filled
+    length (entries past n_visual[b] are -1)."""
+    M = w.coords.shape[1]
+    prefix = int(max(0, min(64, int(np.min(w.cache_len)) - M)))
+    out = np.full((w.B, M), -1, np.int32)
+    for b in range(w.B):
+        n = int(w.n_visual[b])
+        out[b, :n] = prefix + np.arange(n)
+        assert n == 0 or prefix + n - 1 < int(w.cache_len[b])
+    return out
+
+
 def mem_shape(w: Workload) -> tuple:
     return (w.B, w.M_max, w.NL, w.H, w.D)
 
