@@ -499,7 +499,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the rebinding path shards by sequence, KV head or "
-              "layer with no exchange, and this build runs and reports N=1 only.", file=sys.stderr)
+              "layer with no exchange, and only N=1 is run and reported.", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -130,3 +130,53 @@ def test_decode_after_prefill_and_revisit():
         ref = oracle.decode_attention(rope_d, cache_o, layer, npy(q), next_o, res["new_cache_len"],
                                       D ** -0.5, "bf16")
         _check(outs[layer], ref, cache_o, res["new_cache_len"], H, G, "bf16", layer)
+
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_decode_graph_replays_match_eager(paged):
+    """prcr_decode_attention captured in a HIP graph: each replay, after eager work
+    that clobbers the output and the workspace, reproduces the eager result bit for
+    bit (the kernels clear nothing with memsets, so replays are self-contained)."""
+    B, NL, H, D, G, layer = 4, 2, 2, 128, 4, 1
+    lens = np.array([0, 1, 700, 333], np.int32)
+    cap = 800
+    g = torch.Generator().manual_seed(91)
+    rnd = lambda *s: torch.randn(s, generator=g).to(torch.bfloat16)
+    if paged:
+        bs, need = 16, 50
+        table = np.random.default_rng(92).permutation(B * need).astype(np.int32).reshape(B, need)
+        cache = prcr.Cache(rnd(NL, B * need, bs, H, D).to(DEV), rnd(NL, B * need, bs, H, D).to(DEV),
+                           to_dev(table))
+    else:
+        cache = prcr.Cache(rnd(B, NL, H, cap, D).to(DEV), rnd(B, NL, H, cap, D).to(DEV))
+    rope = prcr.Rope(D, (16, 24, 24), False, 1e6)
+    q = rnd(B, H * G, D).to(DEV)
+    q_pos, cl = to_dev(np.array([5, 900, 3000, 17], np.int32)), to_dev(lens)
+    out = torch.empty((B, H * G, D), dtype=torch.float32, device=DEV)
+    ws = torch.empty(prcr.decode_workspace_bytes(cache, B, H * G) // 4 + 1, dtype=torch.float32,
+                     device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    s = torch.cuda.Stream(device=DEV)
+    _say(f"graph capture of decode attention, paged={paged}, 3 replays")
+
+    def call():
+        prcr.decode_attention(rope, cache, layer, q, q_pos, cl, None, out, ws, err, s)
+
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        call()
+    torch.cuda.synchronize()
+    eager = out.clone()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        call()
+    torch.cuda.synchronize()
+    for r in range(3):
+        out.fill_(float("nan"))                     # eager work between replays
+        ws.fill_(float("nan"))
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), f"replay {r}"
+    assert int(err.item()) == 0

@@ -237,3 +237,47 @@ def test_key_only_value_slot_not_filled():
     assert slots[1] == -1 and np.array_equal(slots, ref["slot_mapping"])
     assert np.array_equal(npy(cache.v), ref["v"])
     assert_keys_close(npy(cache.k), ref["k"], "bf16")
+
+
+def test_prefill_graph_replays_match_eager():
+    """One layer of prcr_prefill_capture captured in a HIP graph: each replay, after
+    eager work that restores the cache and the memory to their contents before the
+    call, reproduces the eager result."""
+    pf = Prefill("bf16", 128, (24, 20, 20), True, True, NL=2, H=4)
+    _say("graph capture of prefill capture (paged), 3 replays")
+    mem = prcr.Memory(pf.mem_k.to(DEV), pf.mem_v.to(DEV),
+                      torch.zeros((pf.B, pf.M, 3), dtype=torch.int32, device=DEV),
+                      to_dev(pf.n_visual))
+    cache = prcr.Cache(pf.cache_k.to(DEV), pf.cache_v.to(DEV), to_dev(pf.cache_cfg["block_table"]))
+    rope = prcr.Rope(pf.D, pf.rope["sections"], pf.rope["interleaved"], pf.rope["theta"])
+    rk, rv = pf.raw[1][0].to(DEV), pf.raw[1][1].to(DEV)
+    args = (to_dev(pf.pos), to_dev(pf.n_tokens), to_dev(pf.vis_index))
+    start = torch.zeros(pf.B, dtype=torch.int32, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    s = torch.cuda.Stream(device=DEV)
+
+    def call():
+        prcr.prefill_capture(rope, mem, 1, rk, rv, *args, cache, start, True, err, s)
+
+    outs = (cache.k, cache.v, mem.k, mem.v, mem.coords)
+    before = [t.clone() for t in outs]
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        call()
+    torch.cuda.synchronize()
+    eager = [t.clone() for t in outs]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        call()
+    torch.cuda.synchronize()
+    for r in range(3):
+        for t, t0 in zip(outs, before):
+            t.copy_(t0)                                 # eager work between replays
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(outs, eager):
+            assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a,
+                               b.view(torch.int16) if b.dtype == torch.bfloat16 else b), f"replay {r}"
+    assert int(err.item()) == 0
