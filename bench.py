@@ -363,24 +363,26 @@ def video_revisits(dev, reps=5):
             "total_GBs": round(sum(nbytes) / (sum(med) * 1e6), 1)}
 
 
-def decode_attention_bw(dev, steps=20):
-    """Bandwidth of decode attention over workload 3's active cache after its revisit
-    (32 sequences, lengths + 256, 36 layers x 8 KV heads, 32 query heads, d 128,
-    bf16), one layer per call.  Algorithmic bytes: every attended K and V row once,
-    plus the queries and outputs."""
+def decode_attention_bw(dev, steps=20, cfg=3):
+    """Bandwidth of decode attention over a workload's active cache after its revisit
+    (lengths + K_b), 4 query heads per KV head, bf16, one layer per call: workload 3
+    (32 sequences, 36 layers x 8 KV heads, contiguous) or workload 5 (64 sequences,
+    28 layers x 4 KV heads, paged, block 16).  Algorithmic bytes: every attended K
+    and V row once, plus the queries and outputs."""
     import numpy as np
     import torch
 
     import paper_2606_26631_amd as prcr
     import workloads
-    w = workloads.make(3, "full")
+    w = workloads.make(cfg, "full")
     Hq = 4 * w.H
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
     g = torch.Generator(device=dev)
-    g.manual_seed(4000)
-    shape = (w.B, w.NL, w.H, w.s_max, w.D)
+    g.manual_seed(4000 + cfg)
+    shape = workloads.cache_shape(w)
     cache = prcr.Cache(torch.randn(shape, generator=g, device=dev).to(torch.bfloat16),
-                       torch.randn(shape, generator=g, device=dev).to(torch.bfloat16))
+                       torch.randn(shape, generator=g, device=dev).to(torch.bfloat16),
+                       t(w.block_table) if w.paged else None)
     rope = prcr.Rope(w.D, w.sections, w.interleaved, w.theta)
     lens = (w.cache_len + np.diff(w.sel_off)).astype(np.int32)
     q = torch.randn((w.B, Hq, w.D), generator=g, device=dev).to(torch.bfloat16)
@@ -409,12 +411,15 @@ def decode_attention_bw(dev, steps=20):
     nbytes = int(lens.sum()) * w.H * w.D * 2 * 2 + w.B * Hq * w.D * (2 + 4)
     del cache, ws
     torch.cuda.empty_cache()
-    return {"kernel": "prcr_decode_attention", "workload": f"{w.B} sequences, cache lengths "
-            f"{int(lens.min())}-{int(lens.max())}, {w.H} KV heads, {Hq} query heads, d {w.D}, bf16, "
-            "one layer per call", "mean_call_us": round(mean_s * 1e6, 2),
-            "algorithmic_bytes_per_call": nbytes, "achieved": round(nbytes / mean_s / 1e9, 1),
-            "unit": "GB/s", "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4),
-            "traffic": load_traffic("decode_attention", "decode")}
+    layout = f"paged, block {w.block_size}" if w.paged else "contiguous"
+    res = {"kernel": "prcr_decode_attention", "workload": f"workload {cfg}: {w.B} sequences, cache "
+           f"lengths {int(lens.min())}-{int(lens.max())}, {w.H} KV heads, {Hq} query heads, d {w.D}, "
+           f"bf16, {layout}, one layer per call", "mean_call_us": round(mean_s * 1e6, 2),
+           "algorithmic_bytes_per_call": nbytes, "achieved": round(nbytes / mean_s / 1e9, 1),
+           "unit": "GB/s", "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4)}
+    if cfg == 3:
+        res["traffic"] = load_traffic("decode_attention", "decode")
+    return res
 
 
 def roofline(w, rebind_ms, traffic):
@@ -496,6 +501,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-attention section")
     ap.add_argument("--no-video", action="store_true", help="skip the four-revisit video section")
     ap.add_argument("--no-key-only", action="store_true", help="skip the key-only memory section")
+    ap.add_argument("--no-tp-shard", action="store_true",
+                    help="skip the one-GPU share of the workload at 8-way KV-head parallelism")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the rebinding path shards by sequence, KV head or "
@@ -540,6 +547,12 @@ def main():
             "workload": f"workload {wk.cfg} ({wk.name}), key-only memory: values copied from "
                         "the prompt slots of the same cache",
             "roofline": roofline(wk, rk, None)}
+    if not args.no_tp_shard:
+        wt = workloads.tp_shard(workloads.make(args.workload, "full"), 8)
+        tt, rt, _ = measure(wt, args.steps, args.warmup, dev)
+        out["tp8_shard"] = {"config": describe(wt),
+                            "value": round(wt.entries() * args.steps / (tt / 1e3), 1),
+                            "unit": "entries/s", "roofline": roofline(wt, rt, None)}
     if not args.no_video:
         out["video_revisits"] = video_revisits(dev)
     if not args.no_small_k:
@@ -548,6 +561,7 @@ def main():
         out["prefill_capture"] = prefill_capture_bw(dev)
     if not args.no_decode:
         out["decode_attention"] = decode_attention_bw(dev)
+        out["decode_attention_paged"] = decode_attention_bw(dev, cfg=5)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, dev, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -197,3 +197,17 @@ def test_full_size_key_only_memory(cfg):
     _say(f"  sampled keys bit-exact {exact}/{n}")
     del mem, cache, vals
     torch.cuda.empty_cache()
+
+
+def test_full_size_tp8_shard():
+    """One GPU's share of workload 3 at 8-way KV-head parallelism: 1 KV head, so each
+    (token, layer) row is a single 256-byte row (the small-row regime)."""
+    w = workloads.tp_shard(workloads.make(3, "full"), 8)
+    _say(f"workload 3 full, TP-8 shard: H={w.H} entries={w.entries()}")
+    mem, cache, rope = _prepare(w)
+    rng = np.random.default_rng(38)
+    exact, n, _, _ = _check_call(w, mem, cache, rope, w.sel_off, w.sel_idx, w.p_txt.astype(np.int64),
+                                 w.cache_len.astype(np.int64), rng)
+    _say(f"  sampled keys bit-exact {exact}/{n}")
+    del mem, cache
+    torch.cuda.empty_cache()

@@ -13,8 +13,11 @@ Prefill capture (Eq. (4), (6)-(7)): 32 prompts x 2560 tokens (2048 visual, a
 
 Decode attention (Eq. (14)): the active cache of the 32-sequence workload after
 its revisit (lengths 2801-4246), 8 KV heads, 32 query heads, d 128, bf16, on the
-first and the last layer; sampled (sequence, query head) outputs against the
-oracle, with the tolerance of the small-size tests.
+first and the last layer, and of the paged 64-sequence workload (4 KV heads, 16
+query heads, block 16) on its last layer; sampled (sequence, query head) outputs
+against the oracle, with the tolerance of the small-size tests.  The paged rows
+are gathered through the block table with torch indexing, independently of the
+kernel.
 """
 import numpy as np
 import pytest
@@ -109,17 +112,18 @@ def test_prefill_capture_full_size():
     assert torch.equal(_i16(mem.k[mem_other]), _i16(mem_before)), "another layer's memory changed"
 
 
-@pytest.mark.parametrize("layer", [0, 35])
-def test_decode_attention_full_size(layer):
-    w = workloads.make(3, "full")
+@pytest.mark.parametrize("cfg,layer", [(3, 0), (3, 35), (5, 27)])
+def test_decode_attention_full_size(cfg, layer):
+    w = workloads.make(cfg, "full")
     Hq = 4 * w.H
-    _say(f"decode attention full size: {w.B} sequences, {w.H} KV heads, {Hq} query heads, "
-         f"layer {layer}")
+    _say(f"decode attention full size: workload {cfg}, {w.B} sequences, {w.H} KV heads, "
+         f"{Hq} query heads, layer {layer}, paged={w.paged}")
     g = torch.Generator(device=DEV)
     g.manual_seed(4000 + layer)
-    shape = (w.B, w.NL, w.H, w.s_max, w.D)
+    shape = workloads.cache_shape(w)
     cache = prcr.Cache(torch.randn(shape, generator=g, device=DEV).to(torch.bfloat16),
-                       torch.randn(shape, generator=g, device=DEV).to(torch.bfloat16))
+                       torch.randn(shape, generator=g, device=DEV).to(torch.bfloat16),
+                       to_dev(w.block_table) if w.paged else None)
     rope = prcr.Rope(w.D, w.sections, w.interleaved, w.theta)
     lens = (w.cache_len + np.diff(w.sel_off)).astype(np.int32)
     q = torch.randn((w.B, Hq, w.D), generator=g, device=DEV).to(torch.bfloat16)
@@ -135,17 +139,24 @@ def test_decode_attention_full_size(layer):
     rng = np.random.default_rng(4100 + layer)
     G = Hq // w.H
     worst = 0.0
-    for b in range(w.B):
+    for b in rng.choice(w.B, min(w.B, 32), replace=False):
         n = int(lens[b])
         for qh in rng.choice(Hq, 3, replace=False):
             kvh = int(qh) // G
-            k = workloads.as_numpy_storage(cache.k[b, layer, kvh, :n])
-            v = workloads.as_numpy_storage(cache.v[b, layer, kvh, :n])
+            if w.paged:
+                slots = np.arange(n)
+                blk = torch.from_numpy(w.block_table[b, slots // w.block_size].astype(np.int64)).to(DEV)
+                off = torch.from_numpy((slots % w.block_size).astype(np.int64)).to(DEV)
+                k = workloads.as_numpy_storage(cache.k[layer, blk, off, kvh])
+                v = workloads.as_numpy_storage(cache.v[layer, blk, off, kvh])
+            else:
+                k = workloads.as_numpy_storage(cache.k[b, layer, kvh, :n])
+                v = workloads.as_numpy_storage(cache.v[b, layer, kvh, :n])
             one = {"paged": False, "s_max": n, "k": k[None, None, None], "v": v[None, None, None]}
             ref = oracle.decode_attention(rope_d, one, 0, q_np[b:b + 1, qh:qh + 1], q_pos[b:b + 1],
                                           np.array([n]), w.D ** -0.5, "bf16")[0, 0]
             vmax = np.abs(oracle.storage_to_f64(v, "bf16")).max()
             dmax = np.abs(out[b, qh] - ref).max()
             worst = max(worst, dmax / vmax)
-            assert dmax <= 5e-5 * vmax + 1e-6, (b, int(qh), dmax, vmax)
+            assert dmax <= 5e-5 * vmax + 1e-6, (int(b), int(qh), dmax, vmax)
     _say(f"decode attention: worst |out - ref| / max|V| = {worst:.2e}")

@@ -30,6 +30,7 @@ uses fewer sequences and layers, so the oracle finishes in seconds.
 """
 from __future__ import annotations
 
+import dataclasses
 import math
 from dataclasses import dataclass, field
 
@@ -218,6 +219,14 @@ def make(cfg: int, scale: str = "full", seed: int | None = None) -> Workload:
 # --------------------------------------------------------------------------
 # Tensor contents
 # --------------------------------------------------------------------------
+def tp_shard(w: Workload, tp: int) -> Workload:
+    """One GPU's share of workload w when its KV heads are split over tp GPUs
+    (tensor parallelism): the same sequences, selection and caches with H / tp heads."""
+    if w.H % tp != 0:
+        raise ValueError(f"{w.H} KV heads do not split over {tp} GPUs")
+    return dataclasses.replace(w, H=w.H // tp, name=f"{w.name}-tp{tp}-shard")
+
+
 def value_slots(w: Workload) -> np.ndarray:
     """Value-slot table of a key-only memory for workload w, int32 [B][M_max]: the
     prompt is read as up to 64 text tokens followed by the visual tokens, so visual
