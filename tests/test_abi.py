@@ -17,6 +17,18 @@ HEADER = os.path.join(ROOT, "include", "prcr.h")
 FAKE = 0x10000          # 64 KiB-aligned placeholder address; never dereferenced
 
 
+def _gpu_visible() -> bool:
+    import torch
+    return torch.cuda.device_count() > 0          # counts devices without initialising them
+
+
+# The validation tests below pass placeholder pointers and rely on every call being
+# rejected on the host.  They are host-side checks: where a GPU is visible they are
+# skipped, so that a validation mistake can never turn into a launch on bad memory.
+host_only = pytest.mark.skipif(_gpu_visible(), reason="placeholder-pointer checks run on hosts "
+                                                      "without a GPU")
+
+
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
@@ -87,6 +99,7 @@ def call_store(mem, layer=0, raw_k=FAKE, s_src=10):
                             s_src, FAKE, None, None)
 
 
+@host_only
 def test_rebind_validation_errors():
     rope, mem, cache = good()
     assert call_rebind(None, mem, cache) == 1
@@ -135,6 +148,7 @@ def test_rebind_validation_errors():
     assert call_rebind(r2, m2, c2) == 4
 
 
+@host_only
 def test_reassign_validation_errors():
     _, mem, _ = good()
     assert call_reassign(None) == 1
@@ -147,6 +161,7 @@ def test_reassign_validation_errors():
     assert call_reassign(m2) == 1
 
 
+@host_only
 def test_store_validation_errors():
     _, mem, _ = good()
     assert call_store(None) == 1
@@ -167,6 +182,7 @@ def call_revisit(rope, mem, cache, mode=0, l_ext=2, p_txt=FAKE, next_pos=FAKE + 
                           new_pos, next_pos, new_len, FAKE, None, None)
 
 
+@host_only
 def test_revisit_validation_errors():
     rope, mem, cache = good()
     assert call_revisit(rope, None, cache) == 1
@@ -180,3 +196,86 @@ def test_revisit_validation_errors():
     assert call_revisit(r2, m2, c2) == 1
     r2, m2, c2 = good(); r2.section[0], r2.section[1] = 32, 8
     assert call_revisit(r2, m2, c2) == 6
+
+
+def call_prefill(rope, mem, cache, layer=0, raw_k=FAKE, raw_v=FAKE, s_src=10, pos=FAKE,
+                 n_tokens=FAKE, vis_index=FAKE, write_coords=1, cache_start=FAKE, err=None):
+    L = prcr.lib()
+    return L.prcr_prefill_capture(ctypes.byref(rope) if rope is not None else None,
+                                  ctypes.byref(mem) if mem is not None else None, layer, raw_k,
+                                  raw_v, s_src, pos, n_tokens, vis_index, write_coords,
+                                  ctypes.byref(cache) if cache is not None else None, cache_start,
+                                  err, None)
+
+
+@host_only
+def test_prefill_validation_errors():
+    rope, mem, cache = good()
+    assert call_prefill(None, mem, cache) == 1
+    assert call_prefill(rope, None, cache) == 1
+    assert call_prefill(rope, mem, None) == 1
+    for arg in ("raw_k", "raw_v", "pos", "n_tokens", "vis_index", "cache_start"):
+        assert call_prefill(rope, mem, cache, **{arg: None}) == 1, arg
+    assert call_prefill(rope, mem, cache, layer=28) == 2
+    assert call_prefill(rope, mem, cache, layer=-1) == 2
+    assert call_prefill(rope, mem, cache, s_src=0) == 2
+    assert call_prefill(rope, mem, cache, raw_k=FAKE + 8) == 4
+    assert call_prefill(rope, mem, cache, pos=FAKE + 2) == 4
+    assert call_prefill(rope, mem, cache, err=FAKE + 2) == 4
+    r2, m2, c2 = good(); m2.coords = None
+    assert call_prefill(r2, m2, c2) == 1                 # coordinates requested, none given
+    r2, m2, c2 = good(); m2.v = None
+    assert call_prefill(r2, m2, c2) == 1                 # key-only memory without v_slot
+    r2, m2, c2 = good(); c2.paged = 1
+    assert call_prefill(r2, m2, c2) == 1
+    r2, m2, c2 = good(); m2.head_dim = 64
+    assert call_prefill(r2, m2, c2) == 2
+    r2, m2, c2 = good(); r2.section[0], r2.section[1] = 32, 8
+    assert call_prefill(r2, m2, c2) == 6
+
+
+def call_decode(rope, cache, dtype=1, batch=2, n_layers=28, n_kv=4, layer=0, q=FAKE, n_q=16,
+                q_pos=FAKE, cache_len=FAKE, scale=0.088, out=FAKE, ws=FAKE, ws_bytes=1 << 30,
+                err=None):
+    L = prcr.lib()
+    return L.prcr_decode_attention(ctypes.byref(rope) if rope is not None else None,
+                                   ctypes.byref(cache) if cache is not None else None, dtype,
+                                   batch, n_layers, n_kv, layer, q, n_q, q_pos, cache_len, scale,
+                                   out, ws, ws_bytes, err, None)
+
+
+@host_only
+def test_decode_validation_errors():
+    rope, _, cache = good()
+    assert call_decode(None, cache) == 1
+    assert call_decode(rope, None) == 1
+    for arg in ("q", "q_pos", "cache_len", "out", "ws"):
+        assert call_decode(rope, cache, **{arg: None}) == 1, arg
+    assert call_decode(rope, cache, dtype=5) == 3
+    assert call_decode(rope, cache, batch=0) == 2
+    assert call_decode(rope, cache, n_q=6) == 2             # not a multiple of the KV heads
+    assert call_decode(rope, cache, n_q=36) == 2            # 9 query heads per KV head
+    assert call_decode(rope, cache, layer=28) == 2
+    assert call_decode(rope, cache, scale=float("nan")) == 2
+    assert call_decode(rope, cache, ws_bytes=16) == 2       # workspace too small
+    assert call_decode(rope, cache, q=FAKE + 8) == 4
+    assert call_decode(rope, cache, out=FAKE + 2) == 4
+    r2, _, c2 = good(); r2.head_dim = 96; r2.section[0], r2.section[1], r2.section[2] = 16, 16, 16
+    assert call_decode(r2, c2) == 6                         # head_dim without a kernel
+    r2, _, c2 = good(); c2.paged = 1
+    assert call_decode(r2, c2) == 2                         # paged with zero sizes
+    r2, _, c2 = good(); c2.paged, c2.block_size, c2.max_blocks, c2.n_blocks = 1, 16, 4, 8
+    assert call_decode(r2, c2) == 1                         # paged without a block table
+
+
+def test_decode_workspace_size():
+    L = prcr.lib()
+    _, _, cache = good()
+    n = ctypes.c_size_t(0)
+    assert L.prcr_decode_workspace_size(ctypes.byref(cache), 2, 16, 4, 128, ctypes.byref(n)) == 0
+    # [batch][query heads][splits][head_dim + 2] floats, whole splits
+    per_split = 2 * 16 * (128 + 2) * 4
+    assert n.value > 0 and n.value % per_split == 0
+    assert L.prcr_decode_workspace_size(ctypes.byref(cache), 2, 16, 4, 128, None) == 1
+    assert L.prcr_decode_workspace_size(ctypes.byref(cache), 2, 16, 4, 100, ctypes.byref(n)) == 6
+    assert L.prcr_decode_workspace_size(None, 2, 16, 4, 128, ctypes.byref(n)) == 1
