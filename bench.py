@@ -34,9 +34,10 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 _CSRC = "paper_2606_26631_amd/csrc/"
-_COMMON = [_CSRC + f for f in ("rotary.h", "prcr_internal.h", "api.cpp")]
-# Sources each measured kernel is built from; a committed counter summary
-# applies only while their hash is the one it was taken on.
+_COMMON = [_CSRC + f for f in ("rotary.h", "prcr_internal.h")]
+# Sources each measured kernel and its launch are built from (the host argument
+# checks are not among them); a committed counter summary applies only while
+# their hash is the one it was taken on.
 KERNEL_SOURCES = {
     "rebind": [_CSRC + "rebind.hip", _CSRC + "reassign.hip", _CSRC + "positions.h"] + _COMMON,
     "prefill": [_CSRC + "prefill.hip"] + _COMMON,

@@ -58,6 +58,22 @@ prcr_status check_selection(const prcr_mem *mem, const int32_t *sel_off, const i
   return PRCR_OK;
 }
 
+// The cache descriptor every entry point that touches a cache validates: layout
+// flag, pointers, geometry, alignment.
+prcr_status check_cache(const prcr_cache *cache) {
+  if (cache == nullptr || cache->k == nullptr || cache->v == nullptr) return PRCR_ERR_NULL;
+  if (cache->paged != 0 && cache->paged != 1) return PRCR_ERR_SHAPE;
+  if (cache->paged) {
+    if (cache->block_table == nullptr) return PRCR_ERR_NULL;
+    if (cache->block_size < 1 || cache->max_blocks < 1 || cache->n_blocks < 1) return PRCR_ERR_SHAPE;
+    if (!aligned(cache->block_table, 4)) return PRCR_ERR_ALIGN;
+  } else if (cache->s_max < 1) {
+    return PRCR_ERR_SHAPE;
+  }
+  if (!aligned(cache->k, 16) || !aligned(cache->v, 16)) return PRCR_ERR_ALIGN;
+  return PRCR_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -174,17 +190,10 @@ prcr_status prepare_rebind(const prcr_rope *rope, const prcr_mem *mem, const int
   if (rope->head_dim != mem->head_dim) return PRCR_ERR_SHAPE;
   st = check_selection(mem, sel_off, sel_idx, total_k);
   if (st != PRCR_OK) return st;
-  if (cache == nullptr || cache->k == nullptr || cache->v == nullptr || cache_len == nullptr)
-    return PRCR_ERR_NULL;
-  if (cache->paged != 0 && cache->paged != 1) return PRCR_ERR_SHAPE;
-  if (cache->paged) {
-    if (cache->block_table == nullptr) return PRCR_ERR_NULL;
-    if (cache->block_size < 1 || cache->max_blocks < 1 || cache->n_blocks < 1) return PRCR_ERR_SHAPE;
-    if (!aligned(cache->block_table, 4)) return PRCR_ERR_ALIGN;
-  } else if (cache->s_max < 1) {
-    return PRCR_ERR_SHAPE;
-  }
-  if (!aligned(cache->k, 16) || !aligned(cache->v, 16) || !aligned(cache_len, 4) ||
+  st = check_cache(cache);
+  if (st != PRCR_OK) return st;
+  if (cache_len == nullptr) return PRCR_ERR_NULL;
+  if (!aligned(cache_len, 4) ||
       (new_cache_len != nullptr && !aligned(new_cache_len, 4)) ||
       (slot_mapping != nullptr && !aligned(slot_mapping, 8)) ||
       (err_flag != nullptr && !aligned(err_flag, 4)))
@@ -255,21 +264,14 @@ prcr_status prcr_prefill_capture(const prcr_rope *rope, const prcr_mem *mem, int
   if (st != PRCR_OK) return st;
   if (rope->head_dim != mem->head_dim) return PRCR_ERR_SHAPE;
   if (raw_k == nullptr || raw_v == nullptr || pos == nullptr || n_tokens == nullptr ||
-      vis_index == nullptr || cache == nullptr || cache->k == nullptr || cache->v == nullptr ||
-      cache_start == nullptr)
+      vis_index == nullptr || cache_start == nullptr)
     return PRCR_ERR_NULL;
+  st = check_cache(cache);
+  if (st != PRCR_OK) return st;
   if (layer < 0 || layer >= mem->n_layers || s_src < 1) return PRCR_ERR_SHAPE;
-  if (cache->paged != 0 && cache->paged != 1) return PRCR_ERR_SHAPE;
-  if (cache->paged) {
-    if (cache->block_table == nullptr) return PRCR_ERR_NULL;
-    if (cache->block_size < 1 || cache->max_blocks < 1 || cache->n_blocks < 1) return PRCR_ERR_SHAPE;
-    if (!aligned(cache->block_table, 4)) return PRCR_ERR_ALIGN;
-  } else if (cache->s_max < 1) {
-    return PRCR_ERR_SHAPE;
-  }
   if (!aligned(raw_k, 16) || !aligned(raw_v, 16) || !aligned(pos, 4) || !aligned(n_tokens, 4) ||
-      !aligned(vis_index, 4) || !aligned(cache->k, 16) || !aligned(cache->v, 16) ||
-      !aligned(cache_start, 4) || (err_flag != nullptr && !aligned(err_flag, 4)))
+      !aligned(vis_index, 4) || !aligned(cache_start, 4) ||
+      (err_flag != nullptr && !aligned(err_flag, 4)))
     return PRCR_ERR_ALIGN;
   const AxisMapId map = axis_map_id(*rope);
   if (map == AxisMapId::kUnsupported) return PRCR_ERR_UNSUPPORTED;
@@ -349,16 +351,16 @@ prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache
   int n_split = 0;
   st = decode_shape(cache, batch, n_q_heads, n_kv_heads, rope->head_dim, &n_split);
   if (st != PRCR_OK) return st;
-  if (cache->k == nullptr || cache->v == nullptr || q == nullptr || q_pos == nullptr ||
-      cache_len == nullptr || out == nullptr || workspace == nullptr ||
-      (cache->paged && cache->block_table == nullptr))
+  st = check_cache(cache);
+  if (st != PRCR_OK) return st;
+  if (q == nullptr || q_pos == nullptr || cache_len == nullptr || out == nullptr ||
+      workspace == nullptr)
     return PRCR_ERR_NULL;
   if (n_layers < 1 || layer < 0 || layer >= n_layers || !std::isfinite(scale)) return PRCR_ERR_SHAPE;
   const size_t need = static_cast<size_t>(batch) * n_q_heads * n_split * (rope->head_dim + 2) * sizeof(float);
   if (workspace_bytes < need) return PRCR_ERR_SHAPE;
-  if (!aligned(cache->k, 16) || !aligned(cache->v, 16) || !aligned(q, 16) || !aligned(q_pos, 4) ||
-      !aligned(cache_len, 4) || !aligned(out, 4) || !aligned(workspace, 4) ||
-      (cache->paged && !aligned(cache->block_table, 4)) || (err_flag != nullptr && !aligned(err_flag, 4)))
+  if (!aligned(q, 16) || !aligned(q_pos, 4) || !aligned(cache_len, 4) || !aligned(out, 4) ||
+      !aligned(workspace, 4) || (err_flag != nullptr && !aligned(err_flag, 4)))
     return PRCR_ERR_ALIGN;
   DecodeParams p{};
   p.q = q;
