@@ -604,7 +604,7 @@ def main():
     total_ms, rebind_ms, reassign_ms = measure(w, args.steps, args.warmup, dev)
     ms_step = total_ms / args.steps
     out = {
-        "metric": "rebound KV entries/sec (layers x heads x tokens) and achieved HBM GB/s vs peak",
+        "metric": "rebound KV entries/sec (layers\u00d7heads\u00d7tokens) and achieved HBM GB/s vs peak",
         "value": round(w.entries() * args.steps / (total_ms / 1e3), 1),
         "unit": "entries/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
