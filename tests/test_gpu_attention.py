@@ -180,3 +180,30 @@ def test_decode_graph_replays_match_eager(paged):
         torch.cuda.synchronize()
         assert torch.equal(out, eager), f"replay {r}"
     assert int(err.item()) == 0
+
+
+def test_decode_many_sequences():
+    """3000 sequences (the batch is a grid dimension of the partial kernel) with
+    cache lengths 0-40, paged with block 5, against the oracle."""
+    B, NL, H, D, G, layer, bs = 3000, 2, 1, 64, 2, 1, 5
+    rng = np.random.default_rng(77)
+    lens = rng.integers(0, 41, B).astype(np.int32)
+    need = 9
+    table = rng.permutation(B * need).astype(np.int32).reshape(B, need)
+    g = torch.Generator().manual_seed(78)
+    k = torch.randn((NL, B * need, bs, H, D), generator=g)
+    v = torch.randn((NL, B * need, bs, H, D), generator=g)
+    q = torch.randn((B, H * G, D), generator=g)
+    q_pos = rng.integers(0, 5000, B).astype(np.int32)
+    _say(f"decode attention over {B} sequences, paged block {bs}")
+    cache = prcr.Cache(k.to(DEV), v.to(DEV), to_dev(table))
+    rope = prcr.Rope(D, (8, 12, 12), False, 1e6)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out = prcr.decode_attention(rope, cache, layer, q.to(DEV), to_dev(q_pos), to_dev(lens), err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    cache_o = {"paged": True, "block_size": bs, "block_table": table, "max_blocks": need,
+               "n_blocks": B * need, "k": k.numpy(), "v": v.numpy()}
+    ref = oracle.decode_attention(rope.__dict__ | {"sections": rope.sections}, cache_o, layer,
+                                  q.numpy(), q_pos, lens, D ** -0.5, "f32")
+    _check(out, ref, cache_o, lens, H, G, "f32", layer)

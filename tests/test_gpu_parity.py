@@ -314,3 +314,21 @@ def test_graph_replays_match_eager():
             assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a,
                                b.view(torch.int16) if b.dtype == torch.bfloat16 else b), f"replay {r}"
     assert int(err.item()) == 0
+
+
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("paged", [False, True])
+def test_many_sequences(paged, fused):
+    """3000 sequences of 0-3 selected tokens each (a token's sequence is found by a
+    ballot over all 3001 selection offsets, 47 rounds of 64), against the oracle."""
+    rng = np.random.default_rng(300)
+    B = 3000
+    ks = rng.integers(0, 4, B)
+    lens = rng.integers(0, 21, B)
+    w = workloads.custom(B=B, NL=2, H=1, D=64, dtype="f32", sections=(8, 12, 12), gh=3, gw=4,
+                         ks=tuple(int(k) for k in ks), lens=tuple(int(x) for x in lens),
+                         paged=paged, block_size=5, seed=301)
+    _say(f"{B} sequences, total_k={w.total_k}, paged={paged}, fused={fused}")
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len, fused=fused)
+    assert_parity(case, gpu, ref)
