@@ -626,29 +626,48 @@ def main():
                             "roofline": roofline(w2, r2, load_traffic(f"rebind_workload{w2.cfg}", "rebind"))}
         out["secondary"]["roofline"]["frac_of_copy"] = round(
             out["secondary"]["roofline"]["achieved"] / copy["achieved"], 4)
-    if not args.no_key_only:
+    def key_only():
         wk = workloads.make(args.workload, "full")
         _, rk, _ = measure(wk, args.steps, args.warmup, dev, key_only=True)
-        out["key_only_memory"] = {
-            "workload": f"workload {wk.cfg} ({wk.name}), key-only memory: values copied from "
-                        "the prompt slots of the same cache",
-            "roofline": roofline(wk, rk, None)}
-    if not args.no_tp_shard:
+        return {"workload": f"workload {wk.cfg} ({wk.name}), key-only memory: values copied from "
+                            "the prompt slots of the same cache",
+                "roofline": roofline(wk, rk, None)}
+
+    def tp8_shard():
         wt = workloads.tp_shard(workloads.make(args.workload, "full"), 8)
         tt, rt, _ = measure(wt, args.steps, args.warmup, dev)
-        out["tp8_shard"] = {"config": describe(wt),
-                            "value": round(wt.entries() * args.steps / (tt / 1e3), 1),
-                            "unit": "entries/s", "roofline": roofline(wt, rt, None)}
+        return {"config": describe(wt), "value": round(wt.entries() * args.steps / (tt / 1e3), 1),
+                "unit": "entries/s", "roofline": roofline(wt, rt, None)}
+
+    # Further sections: a Python-level failure in one of them is reported in its
+    # place (traceback on stderr) and does not cost the measurement above.
+    sections = []
+    if not args.no_key_only:
+        sections.append(("key_only_memory", key_only))
+    if not args.no_tp_shard:
+        sections.append(("tp8_shard", tp8_shard))
     if not args.no_video:
-        out["video_revisits"] = video_revisits(dev)
+        sections.append(("video_revisits", lambda: video_revisits(dev)))
     if not args.no_small_k:
-        out["small_k_latency"] = small_k_latency(dev)
-        out["small_workloads"] = small_workloads(dev)
+        sections.append(("small_k_latency", lambda: small_k_latency(dev)))
+        sections.append(("small_workloads", lambda: small_workloads(dev)))
     if not args.no_prefill:
-        out["prefill_capture"] = prefill_capture_bw(dev)
+        sections.append(("prefill_capture", lambda: prefill_capture_bw(dev)))
     if not args.no_decode:
-        out["decode_attention"] = decode_attention_bw(dev)
-        out["decode_attention_paged"] = decode_attention_bw(dev, cfg=5)
+        sections.append(("decode_attention", lambda: decode_attention_bw(dev)))
+        sections.append(("decode_attention_paged", lambda: decode_attention_bw(dev, cfg=5)))
+    for name, fn in sections:
+        try:
+            out[name] = fn()
+        except Exception as e:              # noqa: BLE001 - reported, not hidden
+            import traceback
+            traceback.print_exc()
+            out[name] = {"error": f"{type(e).__name__}: {e}"}
+            try:
+                torch.cuda.synchronize()
+                torch.cuda.empty_cache()
+            except Exception:               # noqa: BLE001 - the error above is the report
+                pass
     if cpu is not None:
         out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
