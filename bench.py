@@ -79,7 +79,7 @@ def load_traffic(name: str, kind: str):
 
 
 class Prepared:
-    def __init__(self, w, dev, key_only=False):
+    def __init__(self, w, dev, key_only=False, mode="pcr"):
         import numpy as np
         import torch
 
@@ -103,10 +103,11 @@ class Prepared:
         self.new_len = torch.empty((w.B,), dtype=torch.int32, device=dev)
         self.slots = torch.empty((w.total_k,), dtype=torch.int64, device=dev)
         self.err = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.mode = mode
 
     def reassign(self, stream):
         import paper_2606_26631_amd as prcr
-        prcr.reassign_coords(self.mem, self.sel_off, self.sel_idx, self.p_txt, "pcr", 2,
+        prcr.reassign_coords(self.mem, self.sel_off, self.sel_idx, self.p_txt, self.mode, 2,
                              self.new_pos, self.next_pos, self.err, stream)
 
     def rebind(self, stream):
@@ -115,9 +116,9 @@ class Prepared:
                            self.cache, self.cache_len, self.new_len, self.slots, self.err, stream)
 
 
-def measure(w, steps, warmup, dev, key_only=False):
+def measure(w, steps, warmup, dev, key_only=False, mode="pcr"):
     import torch
-    p = Prepared(w, dev, key_only)
+    p = Prepared(w, dev, key_only, mode)
     s = torch.cuda.Stream(device=dev)
     torch.cuda.synchronize()
     with torch.cuda.stream(s):
@@ -633,6 +634,15 @@ def main():
                             "the prompt slots of the same cache",
                 "roofline": roofline(wk, rk, None)}
 
+    def shift_mode():
+        ws_ = workloads.make(args.workload, "full")
+        ts, rs, as_ = measure(ws_, args.steps, args.warmup, dev, mode="shift")
+        return {"workload": f"workload {ws_.cfg} ({ws_.name}), SHIFT reassignment (the region "
+                            "translated to start at the next position, layout kept)",
+                "value": round(ws_.entries() * args.steps / (ts / 1e3), 1), "unit": "entries/s",
+                "reassign_mean_us": round(sum(as_) / len(as_) * 1e3, 2),
+                "roofline": roofline(ws_, rs, None)}
+
     def tp8_shard():
         wt = workloads.tp_shard(workloads.make(args.workload, "full"), 8)
         tt, rt, _ = measure(wt, args.steps, args.warmup, dev)
@@ -641,7 +651,7 @@ def main():
 
     # Further sections: a Python-level failure in one of them is reported in its
     # place (traceback on stderr) and does not cost the measurement above.
-    sections = []
+    sections = [("shift_mode", shift_mode)]
     if not args.no_key_only:
         sections.append(("key_only_memory", key_only))
     if not args.no_tp_shard:
