@@ -61,7 +61,17 @@
 extern "C" {
 #endif
 
-typedef enum prcr_status {
+/* The enumerations below are 32-bit integers on both sides of the ABI.  Compiled
+ * as C++ they are given int32_t as their underlying type, so that any 32-bit
+ * value a C caller passes is a representable value the library can reject
+ * (rather than an out-of-range enumeration value). */
+#ifdef __cplusplus
+#define PRCR_ENUM_BASE : int32_t
+#else
+#define PRCR_ENUM_BASE
+#endif
+
+typedef enum prcr_status PRCR_ENUM_BASE {
   PRCR_OK = 0,
   PRCR_ERR_NULL = 1,          /* a required pointer is NULL                        */
   PRCR_ERR_SHAPE = 2,         /* a size or count is out of range or inconsistent   */
@@ -73,10 +83,10 @@ typedef enum prcr_status {
   PRCR_ERR_HIP = 8            /* the HIP runtime reported a launch error           */
 } prcr_status;
 
-typedef enum prcr_dtype { PRCR_F32 = 0, PRCR_BF16 = 1 } prcr_dtype;
+typedef enum prcr_dtype PRCR_ENUM_BASE { PRCR_F32 = 0, PRCR_BF16 = 1 } prcr_dtype;
 
 /* Reassignment rules (Sec. 3.2, Table 2). */
-typedef enum prcr_mode {
+typedef enum prcr_mode PRCR_ENUM_BASE {
   PRCR_MODE_PCR = 0,       /* Position-Consistent Reinsertion, Eq. (8)-(10) (default)    */
   PRCR_MODE_SHIFT = 1,     /* region translated to start at p_txt + 1, layout kept       */
   PRCR_MODE_IDENTITY = 2,  /* original coordinates (direct reuse, Eq. (4))               */

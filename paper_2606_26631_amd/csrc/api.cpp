@@ -22,7 +22,8 @@ prcr_status check_rope(const prcr_rope *rope) {
   const int d = rope->head_dim;
   if (d < 2 || d % 2 != 0 || d / 2 > kMaxPairs) return PRCR_ERR_SHAPE;
   if (rope->section[0] < 0 || rope->section[1] < 0 || rope->section[2] < 0) return PRCR_ERR_SHAPE;
-  if (rope->section[0] + rope->section[1] + rope->section[2] != d / 2) return PRCR_ERR_SHAPE;
+  if (static_cast<int64_t>(rope->section[0]) + rope->section[1] + rope->section[2] != d / 2)
+    return PRCR_ERR_SHAPE;
   if (rope->interleaved != 0 && rope->interleaved != 1) return PRCR_ERR_SHAPE;
   if (!(rope->theta > 0.0) || !std::isfinite(rope->theta)) return PRCR_ERR_SHAPE;
   return PRCR_OK;
@@ -41,6 +42,8 @@ prcr_status check_mem(const prcr_mem *mem, bool need_coords) {
   // Each half row must be a whole number of 16-byte chunks.
   if ((d / 2) * elem_bytes(mem->dtype) % 16 != 0) return PRCR_ERR_SHAPE;
   if (static_cast<int64_t>(mem->n_layers) * mem->n_kv_heads > INT32_MAX / 2) return PRCR_ERR_SHAPE;
+  // One layer's rows of a token (all KV heads) must have a 32-bit byte size.
+  if (static_cast<int64_t>(mem->n_kv_heads) * d * elem_bytes(mem->dtype) > INT32_MAX) return PRCR_ERR_SHAPE;
   if (!aligned(mem->k, 16) || !aligned(mem->v, 16) || !aligned(mem->n_visual, 4))
     return PRCR_ERR_ALIGN;
   if (mem->v == nullptr && !aligned(mem->v_slot, 4)) return PRCR_ERR_ALIGN;

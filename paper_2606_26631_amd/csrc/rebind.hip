@@ -422,30 +422,6 @@ hipError_t dispatch_layout(const RebindParams &p, int head_dim, AxisMapId map, b
 
 }  // namespace
 
-AxisMapId axis_map_id(const prcr_rope &rope) {
-  const int *s = rope.section;
-  if (rope.head_dim == 64) {
-    if (!rope.interleaved && s[0] == 8 && s[1] == 12 && s[2] == 12) return AxisMapId::kS_8_12_12;
-    if (rope.interleaved && s[0] == 11 && s[1] == 11 && s[2] == 10) return AxisMapId::kI_11_11_10;
-  } else if (rope.head_dim == 128) {
-    if (!rope.interleaved && s[0] == 16 && s[1] == 24 && s[2] == 24) return AxisMapId::kS_16_24_24;
-    if (rope.interleaved && s[0] == 22 && s[1] == 21 && s[2] == 21) return AxisMapId::kI_22_21_21;
-    if (rope.interleaved && s[0] == 24 && s[1] == 20 && s[2] == 20) return AxisMapId::kI_24_20_20;
-  }
-  return AxisMapId::kUnsupported;
-}
-
-int axis_of_pair(AxisMapId id, int i) {
-  switch (id) {
-    case AxisMapId::kS_8_12_12: return Sectioned<8, 12, 12>::axis(i);
-    case AxisMapId::kI_11_11_10: return Interleaved<11, 11, 10>::axis(i);
-    case AxisMapId::kS_16_24_24: return Sectioned<16, 24, 24>::axis(i);
-    case AxisMapId::kI_22_21_21: return Interleaved<22, 21, 21>::axis(i);
-    case AxisMapId::kI_24_20_20: return Interleaved<24, 20, 20>::axis(i);
-    default: return -1;
-  }
-}
-
 hipError_t launch_rebind(const RebindParams &p, prcr_dtype dtype, int head_dim, AxisMapId map,
                          bool paged, bool fused, hipStream_t stream) {
   if (dtype == PRCR_F32) return dispatch_layout<float>(p, head_dim, map, paged, fused, stream);
