@@ -184,3 +184,66 @@ def test_each_axis_moves_only_its_pairs(interleaved, sections):
         mask = np.concatenate([axis == a, axis == a])
         assert changed[mask].all() and not changed[~mask].any()
     assert P == len(axis)
+
+
+@pytest.mark.parametrize("interleaved,sections,theta", [(True, (24, 20, 20), 5e6), (False, (16, 24, 24), 1e6)])
+def test_float64_error_within_derived_bound_of_50_digit_reference(interleaved, sections, theta):
+    """The oracle against the rotation evaluated to 50 significant digits.
+
+    The reference takes theta^(-2i/d), the product with the position and the
+    cosine and sine in mpmath, from the same float64 inputs.  The oracle's
+    error budget per output, with u = 2^-53:
+      * inv_freq: 2i/d is exact for a power-of-two d; the power adds at most
+        ~1 ulp, so the angle carries |angle| * 2u;
+      * the product pos * inv_freq rounds once: |angle| * u more;
+      * cos and sin: at most ~1 ulp each, so u in absolute terms;
+      * a*c - b*s: two products and a difference, 3u * (|a| + |b|).
+    Total: (|lo| + |hi|) * ((3 |angle| + 1) u + 3u).  The test allows twice that.
+    A wrong angle, axis, orientation or frequency is off by many orders more.
+    """
+    import mpmath
+    mpmath.mp.dps = 50
+    D = 128
+    P = D // 2
+    invf, axis = inv_freq(theta, D), pair_axis(D, sections, interleaved)
+    x = RNG.standard_normal((6, D))
+    pos = np.concatenate([RNG.uniform(0, 12000, (4, 3)), [[1e-3, 0.5, 3.0]], [[9999.75, 9998.5, 9997.25]]])
+    y = rotate_keys(x, pos, invf, axis)
+    u = 2.0 ** -53
+    th = mpmath.mpf(theta)
+    for n in range(x.shape[0]):
+        for i in range(P):
+            ang = mpmath.mpf(pos[n, axis[i]]) * th ** (-mpmath.mpf(2 * i) / D)
+            c, s = mpmath.cos(ang), mpmath.sin(ang)
+            lo, hi = mpmath.mpf(x[n, i]), mpmath.mpf(x[n, i + P])
+            ref_lo, ref_hi = lo * c - hi * s, hi * c + lo * s
+            bound = 2 * (abs(x[n, i]) + abs(x[n, i + P])) * ((3 * float(abs(ang)) + 1) * u + 3 * u)
+            assert abs(float(y[n, i] - ref_lo)) <= bound, (n, i)
+            assert abs(float(y[n, i + P] - ref_hi)) <= bound, (n, i)
+
+
+@pytest.mark.parametrize("interleaved,sections", [(False, (2, 3, 3)), (True, (3, 3, 2))])
+def test_equals_exponential_of_the_rotation_generator(interleaved, sections):
+    """Eq. (4)'s rotation as a matrix exponential, built without a cosine or sine.
+
+    R(p) = expm(G), where G is skew-symmetric with G[i+d/2, i] = angle_i and
+    G[i, i+d/2] = -angle_i: a rotation by angle_i in the plane (e_i, e_{i+d/2})
+    that turns e_i towards e_{i+d/2}.  scipy's expm evaluates it by scaling and
+    squaring a Pade approximant.  The full d x d product also checks that no
+    other component mixes in.
+    """
+    from scipy.linalg import expm
+    D = 16
+    P = D // 2
+    invf, axis = inv_freq(100.0, D), pair_axis(D, sections, interleaved)
+    for _ in range(5):
+        pos = RNG.uniform(-6, 6, 3)
+        G = np.zeros((D, D))
+        for i in range(P):
+            a = pos[axis[i]] * invf[i]
+            G[i + P, i], G[i, i + P] = a, -a
+        R = expm(G)
+        assert np.allclose(R.T @ R, np.eye(D), atol=1e-12)
+        x = RNG.standard_normal((4, D))
+        assert np.allclose(rotate_keys(x, np.broadcast_to(pos, (4, 3)), invf, axis), x @ R.T,
+                           rtol=0, atol=1e-12)
