@@ -585,6 +585,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-attention section")
     ap.add_argument("--no-video", action="store_true", help="skip the four-revisit video section")
     ap.add_argument("--no-key-only", action="store_true", help="skip the key-only memory section")
+    ap.add_argument("--no-capacity", action="store_true",
+                    help="skip the run with 8192 cache slots per sequence")
     ap.add_argument("--no-tp-shard", action="store_true",
                     help="skip the one-GPU share of the workload at 8-way KV-head parallelism")
     args = ap.parse_args()
@@ -643,6 +645,12 @@ def main():
                 "reassign_mean_us": round(sum(as_) / len(as_) * 1e3, 2),
                 "roofline": roofline(ws_, rs, None)}
 
+    def capacity_8192():
+        wc = workloads.with_capacity(workloads.make(args.workload, "full"), 8192)
+        tc, rc, _ = measure(wc, args.steps, args.warmup, dev)
+        return {"config": describe(wc), "value": round(wc.entries() * args.steps / (tc / 1e3), 1),
+                "unit": "entries/s", "roofline": roofline(wc, rc, None)}
+
     def tp8_shard():
         wt = workloads.tp_shard(workloads.make(args.workload, "full"), 8)
         tt, rt, _ = measure(wt, args.steps, args.warmup, dev)
@@ -652,6 +660,8 @@ def main():
     # Further sections: a Python-level failure in one of them is reported in its
     # place (traceback on stderr) and does not cost the measurement above.
     sections = [("shift_mode", shift_mode)]
+    if args.workload == 3 and not args.no_capacity:
+        sections.append(("power_of_two_capacity", capacity_8192))
     if not args.no_key_only:
         sections.append(("key_only_memory", key_only))
     if not args.no_tp_shard:

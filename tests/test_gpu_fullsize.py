@@ -211,3 +211,17 @@ def test_full_size_tp8_shard():
     _say(f"  sampled keys bit-exact {exact}/{n}")
     del mem, cache
     torch.cuda.empty_cache()
+
+
+def test_full_size_power_of_two_capacity():
+    """Workload 3 with 8192 slots per sequence (2 MiB rows per layer and head), the
+    cache shape that bench.py times beside the tight one."""
+    w = workloads.with_capacity(workloads.make(3, "full"), 8192)
+    _say(f"workload 3 full, s_max {w.s_max}")
+    mem, cache, rope = _prepare(w)
+    rng = np.random.default_rng(39)
+    exact, n, _, _ = _check_call(w, mem, cache, rope, w.sel_off, w.sel_idx, w.p_txt.astype(np.int64),
+                                 w.cache_len.astype(np.int64), rng)
+    _say(f"  sampled keys bit-exact {exact}/{n}")
+    del mem, cache
+    torch.cuda.empty_cache()

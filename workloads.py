@@ -227,6 +227,17 @@ def tp_shard(w: Workload, tp: int) -> Workload:
     return dataclasses.replace(w, H=w.H // tp, name=f"{w.name}-tp{tp}-shard")
 
 
+def with_capacity(w: Workload, s_max: int) -> Workload:
+    """Workload w with a contiguous cache of s_max slots per sequence (the same
+    sequences, selection and lengths; only the row stride of the cache changes)."""
+    if w.paged:
+        raise ValueError("the capacity of a paged cache is its block pool")
+    need = int((w.cache_len.astype(np.int64) + np.diff(w.sel_off)).max())
+    if s_max < need:
+        raise ValueError(f"s_max {s_max} is below the {need} slots the revisit needs")
+    return dataclasses.replace(w, s_max=int(s_max), name=f"{w.name}-smax{s_max}")
+
+
 def value_slots(w: Workload) -> np.ndarray:
     """Value-slot table of a key-only memory for workload w, int32 [B][M_max]: the
     prompt is read as up to 64 text tokens followed by the visual tokens, so visual
