@@ -7,9 +7,14 @@ every input already resident in HBM.  Each step re-injects into the same slots,
 so every step does identical work.
 
 Default workload: 32 sequences x 256 selected tokens, 36 layers x 8 KV heads,
-head_dim 128, bf16, interleaved M-RoPE (theta 5e6), contiguous caches.  The paged
-workload (64 sequences x 512 tokens, 28 layers x 4 heads, block size 16) is
-measured in the same run and reported under "secondary".
+head_dim 128, bf16, interleaved M-RoPE (theta 5e6), contiguous caches of 4256
+slots per sequence.  The paged workload (64 sequences x 512 tokens, 28 layers x 4
+heads, block size 16) is measured in the same run and reported under "secondary".
+Further sections time the same path under SHIFT reassignment, with 8192 cache
+slots per sequence (power_of_two_capacity: 2 MiB cache rows, which the memory
+channels absorb faster), with a key-only memory, at one GPU's share of 8-way
+KV-head parallelism, over four video revisits and at small selections, and time
+the prefill capture and decode attention kernels.
 
 Prints one JSON line.  `value` = rebound (sequence, token, layer, KV-head)
 entries per second over the timed steps.  `roofline` is for the dominant kernel
