@@ -160,3 +160,56 @@ def test_decode_attention_full_size(cfg, layer):
             worst = max(worst, dmax / vmax)
             assert dmax <= 5e-5 * vmax + 1e-6, (int(b), int(qh), dmax, vmax)
     _say(f"decode attention: worst |out - ref| / max|V| = {worst:.2e}")
+
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_decode_attention_long_context(paged):
+    """One sequence of 262,144 keys (the whole capacity), 8 KV heads, 32 query heads,
+    bf16: the split-K path with all of its splits on one sequence, against the
+    oracle on sampled query heads."""
+    n, H, Hq, D, NL, layer = 262144, 8, 32, 128, 1, 0
+    _say(f"decode attention long context: {n} keys, paged={paged}")
+    g = torch.Generator(device=DEV)
+    g.manual_seed(4200 + int(paged))
+    rng = np.random.default_rng(4200 + int(paged))
+    if paged:
+        bs = 16
+        n_blocks = n // bs
+        table = rng.permutation(n_blocks).astype(np.int32)[None]
+        shape = (NL, n_blocks, bs, H, D)
+    else:
+        shape = (1, NL, H, n, D)
+    cache = prcr.Cache(torch.randn(shape, generator=g, device=DEV).to(torch.bfloat16),
+                       torch.randn(shape, generator=g, device=DEV).to(torch.bfloat16),
+                       to_dev(table) if paged else None)
+    rope = prcr.Rope(D, (16, 24, 24), False, 1e6)
+    q = torch.randn((1, Hq, D), generator=g, device=DEV).to(torch.bfloat16)
+    q_pos = np.array([n + 40], np.int32)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out = prcr.decode_attention(rope, cache, layer, q, to_dev(q_pos), to_dev(np.array([n], np.int32)),
+                                err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    out = out.cpu().numpy()
+    q_np = workloads.as_numpy_storage(q)
+    rope_d = {"head_dim": D, "sections": (16, 24, 24), "interleaved": False, "theta": 1e6}
+    for qh in rng.choice(Hq, 4, replace=False):
+        kvh = int(qh) // (Hq // H)
+        if paged:
+            slots = np.arange(n)
+            blk = torch.from_numpy(table[0, slots // bs].astype(np.int64)).to(DEV)
+            off = torch.from_numpy((slots % bs).astype(np.int64)).to(DEV)
+            k = workloads.as_numpy_storage(cache.k[layer, blk, off, kvh])
+            v = workloads.as_numpy_storage(cache.v[layer, blk, off, kvh])
+        else:
+            k = workloads.as_numpy_storage(cache.k[0, layer, kvh])
+            v = workloads.as_numpy_storage(cache.v[0, layer, kvh])
+        one = {"paged": False, "s_max": n, "k": k[None, None, None], "v": v[None, None, None]}
+        ref = oracle.decode_attention(rope_d, one, 0, q_np[:, qh:qh + 1], q_pos, np.array([n]),
+                                      D ** -0.5, "bf16")[0, 0]
+        vmax = np.abs(oracle.storage_to_f64(v, "bf16")).max()
+        dmax = np.abs(out[0, qh] - ref).max()
+        _say(f"  query head {int(qh)}: max |out - ref| = {dmax:.3g} (max |V| {vmax:.3g})")
+        assert dmax <= 5e-5 * vmax + 1e-6, (int(qh), dmax, vmax)
+    del cache
+    torch.cuda.empty_cache()
