@@ -5,9 +5,10 @@
 //   * for visual tokens, write the raw rows into the Raw Visual Evidence Memory,
 //     Eq. (6)-(7) (optionally with the token's coordinates).
 //
-// One wavefront covers 2 x (rows per iteration) consecutive (sequence, token,
-// head) rows of the layer; a lane owns one 16-byte chunk of each half of a row,
-// as in the rebind kernel, and evaluates the cos/sin of its own pairs.
+// One wavefront covers PRCR_PF_ITERS x (rows per iteration) consecutive
+// (sequence, token, head) rows of the layer (8 at bf16, d 128: one token's 8
+// heads); a lane owns one 16-byte chunk of each half of a row, as in the rebind
+// kernel, and evaluates the cos/sin of its own pairs.
 #include <climits>
 #include <cmath>
 
