@@ -259,7 +259,8 @@ def f64_to_storage(y, dtype: str) -> np.ndarray:
     if dtype == "bf16":
         return f64_to_bf16_bits(y)
     if dtype == "f32":
-        return np.asarray(y, dtype=np.float64).astype(np.float32)
+        with np.errstate(over="ignore"):      # beyond the float32 range: +-inf, as IEEE rounds
+            return np.asarray(y, dtype=np.float64).astype(np.float32)
     raise ValueError(dtype)
 
 

@@ -332,3 +332,47 @@ def test_many_sequences(paged, fused):
     case = Case(w)
     gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len, fused=fused)
     assert_parity(case, gpu, ref)
+
+
+@pytest.mark.parametrize("dtype,paged", [("bf16", False), ("bf16", True), ("f32", False)])
+def test_special_values(dtype, paged):
+    """NaN, infinities, the largest finite value (whose rotation overflows), the
+    smallest subnormal and signed zeros in the selected tokens' raw rows.  Values
+    (NaN payloads included) are copied bit for bit; keys follow the oracle: NaN
+    where it has NaN, equal infinities, finite results within the key tolerance."""
+    w = workloads.custom(B=3, NL=2, H=2, dtype=dtype, ks=(4, 1, 6), lens=(5, 17, 2), paged=paged,
+                         block_size=8)
+    vals = workloads.torch_values(w, "cpu")
+    big = 3.3895313892515355e38 if dtype == "bf16" else 3.4028234663852886e38
+    tiny = 9.183549615799121e-41 if dtype == "bf16" else 1.401298464324817e-45
+    k, v = vals["mem_k"], vals["mem_v"]
+    for j in range(w.total_k):
+        b = int(np.searchsorted(w.sel_off, j, side="right") - 1)
+        m = int(w.sel_idx[j])
+        row = k[b, m, j % w.NL, j % w.H]
+        row[3] = float("nan")
+        row[10], row[74] = float("inf"), 1.0
+        row[70] = float("-inf")
+        row[20], row[84] = big, big
+        row[21], row[85] = -big, big
+        row[30] = tiny
+        row[40], row[104] = -0.0, 0.0
+        vrow = v[b, m, (j + 1) % w.NL, (j + 1) % w.H]
+        vrow[5] = float("nan")
+        vrow[6] = float("-inf")
+        vrow[7] = tiny
+    if dtype == "bf16":
+        vb = v.view(torch.int16)
+        vb[0, int(w.sel_idx[0]), 0, 0, 9] = 0x7FC1                     # NaN with a payload
+        vb[0, int(w.sel_idx[0]), 0, 0, 11] = -0x0040                     # 0xFFC0: negative NaN
+    else:
+        vi = v.view(torch.int32)
+        vi[0, int(w.sel_idx[0]), 0, 0, 9] = 0x7FC00001
+        vi[0, int(w.sel_idx[0]), 0, 0, 11] = -0x00400000                 # 0xFFC00000
+    _say(f"special values: {dtype}, paged={paged}, {w.total_k} tokens")
+    case = Case(w, vals)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len)
+    assert np.isnan(oracle.storage_to_f64(ref["k"], dtype)).any()      # the specials reached the keys
+    assert np.isinf(oracle.storage_to_f64(ref["k"], dtype)).any()
+    exact, n = assert_parity(case, gpu, ref)
+    _say(f"  keys equal to the oracle {exact}/{n}")
