@@ -211,7 +211,10 @@ prcr_status prcr_reassign_coords(const prcr_mem *mem,
  * the storage type (round to nearest even); values are copied bit for bit.
  * Compiled axis maps: head_dim 64 with sections [8,12,12] or interleaved
  * [11,11,10]; head_dim 128 with [16,24,24], interleaved [22,21,21] or
- * interleaved [24,20,20]; float32 and bfloat16; contiguous and paged.  With a
+ * interleaved [24,20,20]; and 1-D rotary (every pair on t: sections
+ * [head_dim/2, 0, 0], either reading) for models with a plain rotary embedding,
+ * whose visual tokens carry their 1-D position as t; float32 and bfloat16;
+ * contiguous and paged.  With a
  * key-only memory the value rows come from cache slot v_slot[b][m] of the same
  * sequence (see prcr_mem).
  */

@@ -134,6 +134,8 @@ enum class AxisMapId : int {
   kS_16_24_24 = 2,
   kI_22_21_21 = 3,
   kI_24_20_20 = 4,
+  kS_32_0_0 = 5,     // 1-D rotary, head_dim 64: every pair on the t axis
+  kS_64_0_0 = 6,     // 1-D rotary, head_dim 128
   kUnsupported = -1,
 };
 

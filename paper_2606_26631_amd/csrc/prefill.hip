@@ -187,10 +187,12 @@ hipError_t dispatch_map(const PrefillParams &p, int head_dim, AxisMapId map, hip
   if (head_dim == 64) {
     if (map == AxisMapId::kS_8_12_12) return launch_one<T, 64, Sectioned<8, 12, 12>, kPaged>(p, stream);
     if (map == AxisMapId::kI_11_11_10) return launch_one<T, 64, Interleaved<11, 11, 10>, kPaged>(p, stream);
+    if (map == AxisMapId::kS_32_0_0) return launch_one<T, 64, Sectioned<32, 0, 0>, kPaged>(p, stream);
   } else if (head_dim == 128) {
     if (map == AxisMapId::kS_16_24_24) return launch_one<T, 128, Sectioned<16, 24, 24>, kPaged>(p, stream);
     if (map == AxisMapId::kI_22_21_21) return launch_one<T, 128, Interleaved<22, 21, 21>, kPaged>(p, stream);
     if (map == AxisMapId::kI_24_20_20) return launch_one<T, 128, Interleaved<24, 20, 20>, kPaged>(p, stream);
+    if (map == AxisMapId::kS_64_0_0) return launch_one<T, 128, Sectioned<64, 0, 0>, kPaged>(p, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -399,6 +399,8 @@ hipError_t dispatch_map(const RebindParams &p, int head_dim, AxisMapId map, hipS
       return launch_one<T, 64, Sectioned<8, 12, 12>, kPaged, kFused>(p, stream);
     if (map == AxisMapId::kI_11_11_10)
       return launch_one<T, 64, Interleaved<11, 11, 10>, kPaged, kFused>(p, stream);
+    if (map == AxisMapId::kS_32_0_0)
+      return launch_one<T, 64, Sectioned<32, 0, 0>, kPaged, kFused>(p, stream);
   } else if (head_dim == 128) {
     if (map == AxisMapId::kS_16_24_24)
       return launch_one<T, 128, Sectioned<16, 24, 24>, kPaged, kFused>(p, stream);
@@ -406,6 +408,8 @@ hipError_t dispatch_map(const RebindParams &p, int head_dim, AxisMapId map, hipS
       return launch_one<T, 128, Interleaved<22, 21, 21>, kPaged, kFused>(p, stream);
     if (map == AxisMapId::kI_24_20_20)
       return launch_one<T, 128, Interleaved<24, 20, 20>, kPaged, kFused>(p, stream);
+    if (map == AxisMapId::kS_64_0_0)
+      return launch_one<T, 128, Sectioned<64, 0, 0>, kPaged, kFused>(p, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -53,7 +53,9 @@ def test_status_strings():
 
 ROPES = [(64, (8, 12, 12), False, 1e6), (64, (11, 11, 10), True, 1e6),
          (128, (16, 24, 24), False, 1e6), (128, (22, 21, 21), True, 5e6),
-         (128, (24, 20, 20), True, 5e6)]
+         (128, (24, 20, 20), True, 5e6),
+         # 1-D rotary (every pair on t), under both readings of the sections
+         (64, (32, 0, 0), False, 1e4), (128, (64, 0, 0), False, 1e6), (128, (64, 0, 0), True, 1e6)]
 
 
 @pytest.mark.parametrize("D,sections,inter,theta", ROPES)

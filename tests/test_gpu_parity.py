@@ -83,6 +83,9 @@ COMPILED = [
     ("bf16", 64, (8, 12, 12), False), ("bf16", 64, (11, 11, 10), True),
     ("bf16", 128, (16, 24, 24), False), ("bf16", 128, (22, 21, 21), True),
     ("bf16", 128, (24, 20, 20), True),
+    # 1-D rotary: every pair on t (models without M-RoPE)
+    ("f32", 64, (32, 0, 0), False), ("bf16", 128, (64, 0, 0), False),
+    ("bf16", 128, (64, 0, 0), True),
 ]
 
 
@@ -235,7 +238,7 @@ def test_fused_modes(mode):
 
 @pytest.mark.parametrize("paged", [False, True])
 @pytest.mark.parametrize("dtype,D,sections,inter", [COMPILED[0], COMPILED[4], COMPILED[7],
-                                                    COMPILED[9]])
+                                                    COMPILED[9], COMPILED[11]])
 def test_fused_ragged_edges(dtype, D, sections, inter, paged):
     w = workloads.custom(B=5, NL=3, H=3, D=D, dtype=dtype, sections=sections, interleaved=inter,
                          theta=5e6 if inter else 1e6, frames=2, gh=9, gw=7,

@@ -17,7 +17,8 @@ from gpu_util import DEV, assert_keys_close, to_dev
 pytestmark = pytest.mark.gpu
 
 MAPS = [("f32", 64, (8, 12, 12), False), ("bf16", 128, (16, 24, 24), False),
-        ("bf16", 128, (24, 20, 20), True), ("f32", 128, (22, 21, 21), True)]
+        ("bf16", 128, (24, 20, 20), True), ("f32", 128, (22, 21, 21), True),
+        ("bf16", 128, (64, 0, 0), False)]                     # 1-D rotary
 
 
 def _say(msg):

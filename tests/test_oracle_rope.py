@@ -247,3 +247,26 @@ def test_equals_exponential_of_the_rotation_generator(interleaved, sections):
         x = RNG.standard_normal((4, D))
         assert np.allclose(rotate_keys(x, np.broadcast_to(pos, (4, 3)), invf, axis), x @ R.T,
                            rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("interleaved", [False, True])
+def test_one_dimensional_sections_are_textbook_rope_at_t(interleaved):
+    """Sections [d/2, 0, 0] put every pair on the t axis: plain 1-D RoPE at position
+    t, whatever h and w hold (the rotary form of models without M-RoPE, such as the
+    InternVL3.5 family the paper also evaluates).  Reference: transformers' Llama
+    rotary embedding in float32, so the tolerance is that of float32 angles."""
+    from transformers import LlamaConfig
+    from transformers.models.llama.modeling_llama import LlamaRotaryEmbedding, apply_rotary_pos_emb
+    D, S, theta = 128, 64, 1e6
+    cfg = LlamaConfig(hidden_size=2 * D, num_attention_heads=2, head_dim=D, rope_theta=theta)
+    rot = LlamaRotaryEmbedding(config=cfg)
+    x = RNG.standard_normal((1, 1, S, D))
+    t = np.arange(S, dtype=np.float64)
+    cos, sin = rot(torch.zeros(1, S, D), torch.arange(S)[None])
+    _, ref = apply_rotary_pos_emb(torch.from_numpy(x).float(), torch.from_numpy(x).float(), cos, sin)
+    hw = RNG.uniform(-5000, 5000, (S, 2))
+    pos = np.concatenate([t[:, None], hw], axis=1)
+    axis = pair_axis(D, (D // 2, 0, 0), interleaved)
+    assert (axis == 0).all()
+    ours = rotate_keys(x, pos[None, None], inv_freq(theta, D), axis)
+    assert np.allclose(ours, ref.double().numpy(), rtol=0, atol=2e-5)
