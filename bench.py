@@ -14,7 +14,7 @@ Further sections time the same path under SHIFT reassignment, with 8192 cache
 slots per sequence (power_of_two_capacity: 2 MiB cache rows, which the memory
 channels absorb faster), with a key-only memory, at one GPU's share of 8-way
 KV-head parallelism, over four video revisits and at small selections, and time
-the prefill capture and decode attention kernels.
+the prefill capture, raw-memory store and decode attention kernels.
 
 Prints one JSON line.  `value` = rebound (sequence, token, layer, KV-head)
 entries per second over the timed steps.  `roofline` is for the dominant kernel
@@ -307,6 +307,52 @@ def prefill_capture_bw(dev, steps=20):
             "achieved": round(nbytes / mean_s / 1e9, 1), "unit": "GB/s",
             "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4),
             "traffic": load_traffic("prefill_capture", "prefill")}
+
+
+def store_raw_bw(dev, steps=20):
+    """Bandwidth of prcr_store_raw (one layer per call) at the 32-sequence shape: 32
+    prompts of 2560 rows with 2048 visual tokens, 36 layers x 8 KV heads, d 128,
+    bf16.  Algorithmic bytes per call: read and write the K and V rows of every
+    visual token (4 * H * d * 2 bytes each)."""
+    import numpy as np
+    import torch
+
+    import paper_2606_26631_amd as prcr
+    B, M, S, NL, H, D = 32, 2048, 2560, 36, 8, 128
+    g = torch.Generator(device=dev)
+    g.manual_seed(3500)
+    raw_k = torch.randn((B, S, H, D), generator=g, device=dev).to(torch.bfloat16)
+    raw_v = torch.randn((B, S, H, D), generator=g, device=dev).to(torch.bfloat16)
+    mem = prcr.Memory(torch.empty((B, M, NL, H, D), dtype=torch.bfloat16, device=dev),
+                      torch.empty((B, M, NL, H, D), dtype=torch.bfloat16, device=dev),
+                      torch.zeros((B, M, 3), dtype=torch.int32, device=dev),
+                      torch.full((B,), M, dtype=torch.int32, device=dev))
+    vis = torch.from_numpy(np.broadcast_to(256 + np.arange(M, dtype=np.int32), (B, M)).copy()).to(dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    s = torch.cuda.Stream(device=dev)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        for layer in range(3):
+            prcr.store_raw(mem, layer, raw_k, raw_v, vis, err, s)
+        evs = []
+        for i in range(steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(s)
+            prcr.store_raw(mem, i % NL, raw_k, raw_v, vis, err, s)
+            b.record(s)
+            evs.append((a, b))
+        torch.cuda.synchronize()
+    if int(err.item()) != 0:
+        raise RuntimeError("device reported a data error in the store_raw runs")
+    mean_s = sum(a.elapsed_time(b) for a, b in evs) / len(evs) / 1e3
+    nbytes = B * M * H * D * 2 * 4
+    del mem, raw_k, raw_v
+    torch.cuda.empty_cache()
+    return {"kernel": "prcr_store_raw", "workload": f"{B} prompts x {S} rows ({M} visual), {NL} "
+            f"layers x {H} KV heads, d {D}, bf16, one layer per call",
+            "mean_launch_us": round(mean_s * 1e6, 2), "algorithmic_bytes_per_call": nbytes,
+            "achieved": round(nbytes / mean_s / 1e9, 1), "unit": "GB/s",
+            "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4)}
 
 
 def video_revisits(dev, reps=5):
@@ -678,6 +724,7 @@ def main():
         sections.append(("small_workloads", lambda: small_workloads(dev)))
     if not args.no_prefill:
         sections.append(("prefill_capture", lambda: prefill_capture_bw(dev)))
+        sections.append(("store_raw", lambda: store_raw_bw(dev)))
     if not args.no_decode:
         sections.append(("decode_attention", lambda: decode_attention_bw(dev)))
         sections.append(("decode_attention_paged", lambda: decode_attention_bw(dev, cfg=5)))

@@ -26,16 +26,30 @@ __global__ __launch_bounds__(kWaves * kWave) void store_raw_kernel(const StorePa
   const size_t dst = ((static_cast<size_t>(b) * p.max_visual + m) * p.n_layers + p.layer) * p.row_bytes;
   const char *sk = static_cast<const char *>(p.raw_k) + src;
   char *dk = static_cast<char *>(p.mem_k) + dst;
-  for (int o = lane * 16; o < p.row_bytes; o += kWave * 16) {
-    const u32x4 k = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(sk + o));
-    __builtin_nontemporal_store(k, reinterpret_cast<u32x4 *>(dk + o));
-  }
-  if (p.mem_v == nullptr) return;   // key-only memory
-  const char *sv = static_cast<const char *>(p.raw_v) + src;
-  char *dv = static_cast<char *>(p.mem_v) + dst;
-  for (int o = lane * 16; o < p.row_bytes; o += kWave * 16) {
-    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(sv + o));
-    __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(dv + o));
+  const bool with_v = p.mem_v != nullptr;   // false for a key-only memory
+  const char *sv = with_v ? static_cast<const char *>(p.raw_v) + src : nullptr;
+  char *dv = with_v ? static_cast<char *>(p.mem_v) + dst : nullptr;
+  // Up to kBatch 16-byte chunks of each array per lane in flight: every load of
+  // the batch is issued before its stores.
+  constexpr int kBatch = 2;
+  for (int o0 = lane * 16; o0 < p.row_bytes; o0 += kWave * 16 * kBatch) {
+    u32x4 k[kBatch], v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int o = o0 + u * kWave * 16;
+      if (o < p.row_bytes) {
+        k[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(sk + o));
+        if (with_v) v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(sv + o));
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int o = o0 + u * kWave * 16;
+      if (o < p.row_bytes) {
+        __builtin_nontemporal_store(k[u], reinterpret_cast<u32x4 *>(dk + o));
+        if (with_v) __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4 *>(dv + o));
+      }
+    }
   }
 }
 
