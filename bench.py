@@ -47,6 +47,7 @@ KERNEL_SOURCES = {
     "rebind": [_CSRC + "rebind.hip", _CSRC + "reassign.hip", _CSRC + "positions.h"] + _COMMON,
     "prefill": [_CSRC + "prefill.hip"] + _COMMON,
     "decode": [_CSRC + "decode.hip"] + _COMMON,
+    "store": [_CSRC + "store_raw.hip"] + _COMMON,
 }
 
 
@@ -352,7 +353,8 @@ def store_raw_bw(dev, steps=20):
             f"layers x {H} KV heads, d {D}, bf16, one layer per call",
             "mean_launch_us": round(mean_s * 1e6, 2), "algorithmic_bytes_per_call": nbytes,
             "achieved": round(nbytes / mean_s / 1e9, 1), "unit": "GB/s",
-            "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4)}
+            "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4),
+            "traffic": load_traffic("store_raw", "store")}
 
 
 def video_revisits(dev, reps=5):
