@@ -11,7 +11,7 @@ using namespace prcr;
 
 namespace {
 
-constexpr int32_t kVersion = 1 * 10000 + 1 * 100 + 0;
+constexpr int32_t kVersion = 1 * 10000 + 2 * 100 + 0;
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
