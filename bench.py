@@ -12,7 +12,8 @@ slots per sequence.  The paged workload (64 sequences x 512 tokens, 28 layers x 
 heads, block size 16) is measured in the same run and reported under "secondary".
 Further sections time the same path under SHIFT reassignment, with 8192 cache
 slots per sequence (power_of_two_capacity: 2 MiB cache rows, which the memory
-channels absorb faster), with a key-only memory, at one GPU's share of 8-way
+channels absorb faster), with a key-only memory, with 1-D rotary positions (the
+rotary form of InternVL3.5, the paper's other model family), at one GPU's share of 8-way
 KV-head parallelism, over four video revisits and at small selections, and time
 the prefill capture, raw-memory store and decode attention kernels.
 
@@ -640,6 +641,8 @@ def main():
     ap.add_argument("--no-key-only", action="store_true", help="skip the key-only memory section")
     ap.add_argument("--no-capacity", action="store_true",
                     help="skip the run with 8192 cache slots per sequence")
+    ap.add_argument("--no-one-d", action="store_true",
+                    help="skip the run with 1-D rotary positions (InternVL3.5-style)")
     ap.add_argument("--no-tp-shard", action="store_true",
                     help="skip the one-GPU share of the workload at 8-way KV-head parallelism")
     args = ap.parse_args()
@@ -704,6 +707,12 @@ def main():
         return {"config": describe(wc), "value": round(wc.entries() * args.steps / (tc / 1e3), 1),
                 "unit": "entries/s", "roofline": roofline(wc, rc, None)}
 
+    def one_d_rotary():
+        w1 = workloads.one_d(workloads.make(args.workload, "full"))
+        t1, r1, _ = measure(w1, args.steps, args.warmup, dev)
+        return {"config": describe(w1), "value": round(w1.entries() * args.steps / (t1 / 1e3), 1),
+                "unit": "entries/s", "roofline": roofline(w1, r1, None)}
+
     def tp8_shard():
         wt = workloads.tp_shard(workloads.make(args.workload, "full"), 8)
         tt, rt, _ = measure(wt, args.steps, args.warmup, dev)
@@ -717,6 +726,8 @@ def main():
         sections.append(("power_of_two_capacity", capacity_8192))
     if not args.no_key_only:
         sections.append(("key_only_memory", key_only))
+    if not args.no_one_d:
+        sections.append(("one_d_rotary", one_d_rotary))
     if not args.no_tp_shard:
         sections.append(("tp8_shard", tp8_shard))
     if not args.no_video:

@@ -225,3 +225,17 @@ def test_full_size_power_of_two_capacity():
     _say(f"  sampled keys bit-exact {exact}/{n}")
     del mem, cache
     torch.cuda.empty_cache()
+
+
+def test_full_size_one_d_rotary():
+    """Workload 3's shapes with 1-D rotary positions (every pair on t, each visual
+    token's position in t): the form of InternVL3.5's language model."""
+    w = workloads.one_d(workloads.make(3, "full"))
+    _say(f"workload 3 full, 1-D rotary {w.sections}")
+    mem, cache, rope = _prepare(w)
+    rng = np.random.default_rng(40)
+    exact, n, _, _ = _check_call(w, mem, cache, rope, w.sel_off, w.sel_idx, w.p_txt.astype(np.int64),
+                                 w.cache_len.astype(np.int64), rng)
+    _say(f"  sampled keys bit-exact {exact}/{n}")
+    del mem, cache
+    torch.cuda.empty_cache()

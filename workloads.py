@@ -227,6 +227,16 @@ def tp_shard(w: Workload, tp: int) -> Workload:
     return dataclasses.replace(w, H=w.H // tp, name=f"{w.name}-tp{tp}-shard")
 
 
+def one_d(w: Workload) -> Workload:
+    """Workload w for a model with plain 1-D rotary positions (InternVL3.5's language
+    model: every rotary pair on one axis): the same shapes and selection, each visual
+    token's 1-D position m in t, h = w = 0, and the all-t axis map."""
+    coords = np.zeros_like(w.coords)
+    coords[:, :, 0] = np.arange(w.coords.shape[1], dtype=np.int32)[None, :]
+    return dataclasses.replace(w, coords=coords, sections=(w.D // 2, 0, 0), interleaved=False,
+                               theta=1e6, name=f"{w.name.split('-')[0]}-1d-rotary")
+
+
 def with_capacity(w: Workload, s_max: int) -> Workload:
     """Workload w with a contiguous cache of s_max slots per sequence (the same
     sequences, selection and lengths; only the row stride of the cache changes)."""
