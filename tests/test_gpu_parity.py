@@ -2,7 +2,7 @@
 
 Bit-exact: new positions, next text positions, slot mapping, new cache lengths,
 value rows and every cache byte outside the new slots.  Keys: within 1 bf16 ulp
-(bfloat16) or 1e-5 of the rotary pair's norm (float32).  Each test prints what it
+(bfloat16) or 1e-5 relative, element by element (float32).  Each test prints what it
 runs before touching the GPU.
 """
 import numpy as np
