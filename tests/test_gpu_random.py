@@ -1,0 +1,109 @@
+"""Randomized GPU parity: many small configurations drawn from a fixed seed.
+
+Each draws:
+* the storage type, head dimension and axis map (every compiled map, 1-D included);
+* a contiguous or paged cache, with block sizes from 1 to 32;
+* the sequence, layer and head counts;
+* the visual grid (with frames), the per-sequence selection sizes (empty included) and
+  the cache lengths;
+* the reassignment rule, the left extension, and the two-call or fused path.
+
+Each configuration is checked against the oracle to the parity bar: bit-exact
+positions, slots, lengths and values, keys within the key tolerance.  Decode
+attention gets random configurations of its own (grouped-query ratio, lengths,
+capacity, layout), checked to the decode tolerance."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_26631_amd as prcr
+import workloads
+from gpu_util import DEV, Case, assert_parity, run_both, to_dev
+
+pytestmark = pytest.mark.gpu
+
+MAPS = {64: [((8, 12, 12), False), ((11, 11, 10), True), ((32, 0, 0), False)],
+        128: [((16, 24, 24), False), ((22, 21, 21), True), ((24, 20, 20), True),
+              ((64, 0, 0), False), ((64, 0, 0), True)]}
+MODES = ["pcr", "shift", "identity", "lpa", "uir"]
+
+
+def _draw(seed):
+    r = np.random.default_rng(seed)
+    D = int(r.choice([64, 128]))
+    sections, inter = MAPS[D][int(r.integers(len(MAPS[D])))]
+    B = int(r.integers(1, 7))
+    frames, gh, gw = int(r.integers(1, 4)), int(r.integers(1, 10)), int(r.integers(1, 10))
+    M = frames * gh * gw
+    ks = tuple(int(r.integers(0, min(M, 40) + 1)) for _ in range(B))
+    lens = tuple(int(r.integers(0, 61)) for _ in range(B))
+    paged = bool(r.integers(2))
+    w = workloads.custom(B=B, NL=int(r.integers(1, 5)), H=int(r.integers(1, 6)), D=D,
+                         dtype=str(r.choice(["f32", "bf16"])), sections=sections, interleaved=inter,
+                         theta=float(r.choice([1e4, 1e6, 5e6])), frames=frames, gh=gh, gw=gw,
+                         ks=ks, lens=lens, paged=paged, block_size=int(r.choice([1, 3, 16, 32])),
+                         seed=seed)
+    return w, str(r.choice(MODES)), int(r.integers(0, 5)), bool(r.integers(2))
+
+
+@pytest.mark.parametrize("seed", range(9000, 9200))
+def test_random_configuration(seed):
+    w, mode, l_ext, fused = _draw(seed)
+    print(f"seed {seed}: {w.dtype} D={w.D} {w.sections} inter={w.interleaved} B={w.B} NL={w.NL} "
+          f"H={w.H} M={w.M_max} K={list(np.diff(w.sel_off))} paged={w.paged} "
+          f"bs={w.block_size} mode={mode} L={l_ext} fused={fused}", flush=True)
+    case = Case(w)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len, mode=mode, l_ext=l_ext,
+                        fused=fused)
+    assert_parity(case, gpu, ref)
+
+
+@pytest.mark.parametrize("seed", range(9500, 9540))
+def test_random_decode_configuration(seed):
+    r = np.random.default_rng(seed)
+    D = int(r.choice([64, 128]))
+    sections, inter = MAPS[D][int(r.integers(len(MAPS[D])))]
+    dtype = str(r.choice(["f32", "bf16"]))
+    B, H, G, NL = int(r.integers(1, 6)), int(r.integers(1, 4)), int(r.choice([1, 2, 3, 4, 7, 8])), 2
+    layer = int(r.integers(NL))
+    cap = int(r.integers(1, 400))
+    lens = r.integers(0, cap + 1, B).astype(np.int32)
+    paged = bool(r.integers(2))
+    print(f"seed {seed}: decode {dtype} D={D} {sections} B={B} H={H} G={G} cap={cap} "
+          f"lens={lens.tolist()} paged={paged}", flush=True)
+    g = torch.Generator().manual_seed(seed)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    rnd = lambda *shape: (torch.randn(shape, generator=g) * float(r.choice([0.1, 1.0, 2.0]))).to(tdt)
+    if paged:
+        bs = int(r.choice([1, 5, 16]))
+        need = (cap + bs - 1) // bs
+        n_blocks = B * need + int(r.integers(0, 4))
+        table = r.permutation(n_blocks)[:B * need].astype(np.int32).reshape(B, need)
+        k, v = rnd(NL, n_blocks, bs, H, D), rnd(NL, n_blocks, bs, H, D)
+        cache_o = {"paged": True, "block_size": bs, "block_table": table, "max_blocks": need,
+                   "n_blocks": n_blocks}
+    else:
+        k, v = rnd(B, NL, H, cap, D), rnd(B, NL, H, cap, D)
+        cache_o = {"paged": False, "s_max": cap}
+    cache_o["k"], cache_o["v"] = workloads.as_numpy_storage(k), workloads.as_numpy_storage(v)
+    q = rnd(B, H * G, D)
+    q_pos = r.integers(0, 100000, B).astype(np.int32)
+    cache = prcr.Cache(k.to(DEV), v.to(DEV), to_dev(cache_o["block_table"]) if paged else None)
+    rope = prcr.Rope(D, sections, inter, 1e6)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out = prcr.decode_attention(rope, cache, layer, q.to(DEV), to_dev(q_pos), to_dev(lens), err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    ref = oracle.decode_attention(rope.__dict__ | {"sections": rope.sections}, cache_o, layer,
+                                  workloads.as_numpy_storage(q), q_pos, lens, D ** -0.5, dtype)
+    out = out.cpu().numpy()
+    for b in range(B):
+        n = int(lens[b])
+        for kvh in range(H):
+            vmax = np.abs(oracle.storage_to_f64(oracle.cache_rows(cache_o, layer, b, kvh, n, "v"),
+                                                dtype)).max() if n else 0.0
+            for gg in range(G):
+                qh = kvh * G + gg
+                d = np.abs(out[b, qh] - ref[b, qh]).max()
+                assert d <= 5e-5 * vmax + 1e-6, (b, qh, d, vmax)
