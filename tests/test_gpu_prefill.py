@@ -26,8 +26,9 @@ def _say(msg):
 
 
 class Prefill:
-    def __init__(self, dtype, D, sections, inter, paged, NL=3, H=3, seed=5, key_only=False):
-        self.pos, self.vis_index, self.n_tokens, self.n_visual = workloads.prompt()
+    def __init__(self, dtype, D, sections, inter, paged, NL=3, H=3, seed=5, key_only=False,
+                 prompt=None, block_size=4):
+        self.pos, self.vis_index, self.n_tokens, self.n_visual = workloads.prompt(**(prompt or {}))
         B, S = self.vis_index.shape
         M = int(self.n_visual.max()) + 2
         self.B, self.S, self.M, self.NL, self.H, self.D, self.dtype = B, S, M, NL, H, D, dtype
@@ -42,7 +43,7 @@ class Prefill:
         self.key_only = key_only
         self.paged = paged
         if paged:
-            bs = 4
+            bs = block_size
             need = [(int(n) + 16 + bs - 1) // bs for n in self.n_tokens]
             rng = np.random.default_rng(seed)
             table = np.full((B, max(need)), -1, np.int32)

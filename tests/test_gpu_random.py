@@ -11,7 +11,8 @@ Each draws:
 Each configuration is checked against the oracle to the parity bar: bit-exact
 positions, slots, lengths and values, keys within the key tolerance.  Decode
 attention gets random configurations of its own (grouped-query ratio, lengths,
-capacity, layout), checked to the decode tolerance."""
+capacity, layout), checked to the decode tolerance, and so does the prefill capture
+(prompt mixes of text and images or video frames, cache offsets, key-only memory)."""
 import numpy as np
 import pytest
 import torch
@@ -20,6 +21,7 @@ import oracle
 import paper_2606_26631_amd as prcr
 import workloads
 from gpu_util import DEV, Case, assert_parity, run_both, to_dev
+from test_gpu_prefill import Prefill, _compare
 
 pytestmark = pytest.mark.gpu
 
@@ -107,3 +109,25 @@ def test_random_decode_configuration(seed):
                 qh = kvh * G + gg
                 d = np.abs(out[b, qh] - ref[b, qh]).max()
                 assert d <= 5e-5 * vmax + 1e-6, (b, qh, d, vmax)
+
+
+@pytest.mark.parametrize("seed", range(9700, 9730))
+def test_random_prefill_configuration(seed):
+    r = np.random.default_rng(seed)
+    D = int(r.choice([64, 128]))
+    sections, inter = MAPS[D][int(r.integers(len(MAPS[D])))]
+    B = int(r.integers(1, 4))
+    prompt = {"B": B, "n_before": tuple(int(x) for x in r.integers(0, 12, B)),
+              "grid": tuple((int(r.integers(1, 7)), int(r.integers(1, 7))) for _ in range(B)),
+              "n_after": tuple(int(x) for x in r.integers(0, 9, B)),
+              "frames": tuple(int(x) for x in r.integers(1, 4, B))}
+    dtype = str(r.choice(["f32", "bf16"]))
+    paged, key_only = bool(r.integers(2)), bool(r.integers(2))
+    pf = Prefill(dtype, D, sections, inter, paged, NL=int(r.integers(1, 4)), H=int(r.integers(1, 5)),
+                 seed=seed, key_only=key_only, prompt=prompt, block_size=int(r.choice([1, 4, 16])))
+    start = r.integers(0, 17, pf.B).astype(np.int32)
+    print(f"seed {seed}: prefill {dtype} D={D} {sections} inter={inter} prompt={prompt} "
+          f"NL={pf.NL} H={pf.H} paged={paged} key_only={key_only} start={start.tolist()}", flush=True)
+    mem, cache, rope, err = pf.run_gpu(start=start)
+    ref_mem, ref_cache, ref_err = pf.run_oracle(start=start)
+    _compare(pf, mem, cache, err, ref_mem, ref_cache, ref_err)
