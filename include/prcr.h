@@ -91,7 +91,10 @@ typedef enum prcr_mode PRCR_ENUM_BASE {
   PRCR_MODE_SHIFT = 1,     /* region translated to start at p_txt + 1, layout kept       */
   PRCR_MODE_IDENTITY = 2,  /* original coordinates (direct reuse, Eq. (4))               */
   PRCR_MODE_LPA = 3,       /* Linear Position Appending: p_txt + j                       */
-  PRCR_MODE_UIR = 4        /* Uniform Interval Reinsertion: p_txt + j / (K + 1)          */
+  PRCR_MODE_UIR = 4,       /* Uniform Interval Reinsertion: p_txt + j / (K + 1)          */
+  PRCR_MODE_PCR_RIGHT = 5  /* PCR re-anchored rightward (the direction ablation, Sec. 4):
+                              Eq. (10) with p_txt + 1 in place of p_txt - L, so entries lie
+                              in (p_txt + 1, p_txt + L + 2); next text position p_txt + 1 */
 } prcr_mode;
 
 /* Device-side data error bits (OR-ed into *err_flag). */

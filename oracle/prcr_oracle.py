@@ -60,7 +60,7 @@ from fractions import Fraction
 
 import numpy as np
 
-MODES = ("pcr", "shift", "identity", "lpa", "uir")
+MODES = ("pcr", "shift", "identity", "lpa", "uir", "pcr_right")
 
 # Error bits reported through the err word (bitwise OR of these).
 ERR_INDEX = 1      # selected index outside [0, n_visual[b])
@@ -161,7 +161,10 @@ def reassign(coords_sel, p_txt: int, mode: str = "pcr", l_ext: int = 2, valid=No
                 top = v if top is None else max(top, v)
         return out, (p_txt + 1 if top is None else top + 1)
 
-    # PCR, Eq. (9)-(10), exact rational arithmetic, one rounding to float64.
+    # PCR, Eq. (9)-(10), exact rational arithmetic, one rounding to float64.  The
+    # interval starts at p_txt - L (leftward, the paper's default) or, re-anchored
+    # rightward (reading R6), at p_txt + 1.
+    start = p_txt + 1 if mode == "pcr_right" else p_txt - L
     for j in range(K):
         if not ok[j]:
             continue
@@ -170,7 +173,7 @@ def reassign(coords_sel, p_txt: int, mode: str = "pcr", l_ext: int = 2, valid=No
                 u = Fraction(int(c[j, a]) - lo[a], hi[a] - lo[a])       # Eq. (9)
             else:
                 u = Fraction(1, 2)                                        # R2
-            p = (p_txt - L) + (L + 1) * (1 + (K - 1) * u) / Fraction(K + 1)  # Eq. (10)
+            p = start + (L + 1) * (1 + (K - 1) * u) / Fraction(K + 1)     # Eq. (10)
             out[j, a] = float(p)
     return out, p_txt + 1
 

@@ -15,7 +15,7 @@ from ctypes import POINTER, c_double, c_int, c_int32, c_void_p
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libprcr.so")
 
 PRCR_F32, PRCR_BF16 = 0, 1
-MODES = {"pcr": 0, "shift": 1, "identity": 2, "lpa": 3, "uir": 4}
+MODES = {"pcr": 0, "shift": 1, "identity": 2, "lpa": 3, "uir": 4, "pcr_right": 5}
 DERR_INDEX, DERR_CAPACITY, DERR_BLOCK, DERR_OFFSETS, DERR_RANGE = 1, 2, 4, 8, 16
 STATUS = {0: "PRCR_OK", 1: "PRCR_ERR_NULL", 2: "PRCR_ERR_SHAPE", 3: "PRCR_ERR_DTYPE",
           4: "PRCR_ERR_ALIGN", 5: "PRCR_ERR_MODE", 6: "PRCR_ERR_UNSUPPORTED",

@@ -11,7 +11,7 @@ using namespace prcr;
 
 namespace {
 
-constexpr int32_t kVersion = 1 * 10000 + 2 * 100 + 0;
+constexpr int32_t kVersion = 1 * 10000 + 3 * 100 + 0;
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -156,7 +156,7 @@ prcr_status prcr_reassign_coords(const prcr_mem *mem, const int32_t *sel_off, co
   if (st != PRCR_OK) return st;
   if (p_txt == nullptr || next_pos == nullptr) return PRCR_ERR_NULL;
   if (total_k > 0 && new_pos == nullptr) return PRCR_ERR_NULL;
-  if (mode < PRCR_MODE_PCR || mode > PRCR_MODE_UIR || l_ext < 0) return PRCR_ERR_MODE;
+  if (mode < PRCR_MODE_PCR || mode > PRCR_MODE_PCR_RIGHT || l_ext < 0) return PRCR_ERR_MODE;
   if (!aligned(p_txt, 4) || !aligned(next_pos, 4) || (new_pos != nullptr && !aligned(new_pos, 8)) ||
       (err_flag != nullptr && !aligned(err_flag, 4)))
     return PRCR_ERR_ALIGN;
@@ -404,7 +404,7 @@ prcr_status prcr_revisit(const prcr_rope *rope, const prcr_mem *mem, const int32
                                         new_cache_len, slot_mapping, err_flag, true, &p, &map);
   if (st != PRCR_OK) return st;
   if (p_txt == nullptr || next_pos == nullptr) return PRCR_ERR_NULL;
-  if (mode < PRCR_MODE_PCR || mode > PRCR_MODE_UIR || l_ext < 0) return PRCR_ERR_MODE;
+  if (mode < PRCR_MODE_PCR || mode > PRCR_MODE_PCR_RIGHT || l_ext < 0) return PRCR_ERR_MODE;
   if (!aligned(p_txt, 4) || !aligned(next_pos, 4) || (new_pos != nullptr && !aligned(new_pos, 8)))
     return PRCR_ERR_ALIGN;
   p.coords = mem->coords;

@@ -12,14 +12,14 @@ namespace prcr {
 
 constexpr double kExactLimit = 4503599627370496.0;   // 2^52
 
-// PCR along one axis: (p_txt - L) + (L + 1)(1 + (K - 1) u)/(K + 1) with
-// u = (c - lo)/(hi - lo), or u = 1/2 when hi == lo.  Formed as an integer
-// numerator and denominator and divided once in double, which is the correctly
-// rounded value of the rational while both stay below 2^52; beyond that a close
-// double approximation is returned and *range_bad is set.
-__device__ __forceinline__ double pcr_position(int64_t p_txt, int64_t L, int64_t K, int64_t lo,
+// PCR along one axis: A + (L + 1)(1 + (K - 1) u)/(K + 1) with A = p_txt - L
+// (leftward, Eq. (10)) or A = p_txt + 1 (rightward), u = (c - lo)/(hi - lo), or
+// u = 1/2 when hi == lo.  Formed as an integer numerator and denominator and
+// divided once in double, which is the correctly rounded value of the rational
+// while both stay below 2^52; beyond that a close double approximation is
+// returned and *range_bad is set.
+__device__ __forceinline__ double pcr_position(int64_t A, int64_t L, int64_t K, int64_t lo,
                                                int64_t hi, int64_t c, bool *range_bad) {
-  const int64_t A = p_txt - L;
   const int64_t span = hi - lo;
   if (span <= 0) {
     // u = 1/2:  A + (L + 1)/2 = (2A + L + 1) / 2
@@ -64,8 +64,10 @@ __device__ __forceinline__ double reassigned(int mode, int64_t p_txt, int64_t L,
       }
       return static_cast<double>(p_txt * (K + 1) + j + 1) / static_cast<double>(K + 1);
     }
+    case PRCR_MODE_PCR_RIGHT:
+      return pcr_position(p_txt + 1, L, K, lo, hi, c, range_bad);
     default:
-      return pcr_position(p_txt, L, K, lo, hi, c, range_bad);
+      return pcr_position(p_txt - L, L, K, lo, hi, c, range_bad);
   }
 }
 

@@ -27,7 +27,8 @@ MUTS = [
  ("pcr K-1", "(1 + (K - 1) * u)", "(1 + K * u)"),
  ("pcr L+1", "(L + 1) * (1 + (K - 1) * u)", "L * (1 + (K - 1) * u)"),
  ("pcr K+1", "/ Fraction(K + 1)", "/ Fraction(K)"),
- ("pcr anchor", "p = (p_txt - L) +", "p = (p_txt - L + 1) +"),
+ ("pcr anchor", "start = p_txt + 1 if mode == \"pcr_right\" else p_txt - L", "start = p_txt + 1 if mode == \"pcr_right\" else p_txt - L + 1"),
+ ("pcr right anchor", "start = p_txt + 1 if mode == \"pcr_right\" else p_txt - L", "start = p_txt if mode == \"pcr_right\" else p_txt - L"),
  ("R2 midpoint", "u = Fraction(1, 2)", "u = Fraction(0)"),
  ("u denom", "Fraction(int(c[j, a]) - lo[a], hi[a] - lo[a])", "Fraction(int(c[j, a]) - lo[a], hi[a] - lo[a] + 1)"),
  ("shift start", "v = (p_txt + 1) + (int(c[j, a]) - lo[a])", "v = p_txt + (int(c[j, a]) - lo[a])"),

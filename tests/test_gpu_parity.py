@@ -57,7 +57,7 @@ def test_video_four_revisits():
     assert (lens <= w.s_max).all()
 
 
-@pytest.mark.parametrize("mode", ["pcr", "shift", "identity", "lpa", "uir"])
+@pytest.mark.parametrize("mode", ["pcr", "shift", "identity", "lpa", "uir", "pcr_right"])
 @pytest.mark.parametrize("cfg", [1, 3])
 def test_modes(cfg, mode):
     w = workloads.make(cfg, "small")
@@ -226,7 +226,7 @@ def test_fused_workload_small(cfg):
     assert_parity(case, gpu, ref)
 
 
-@pytest.mark.parametrize("mode", ["pcr", "shift", "identity", "lpa", "uir"])
+@pytest.mark.parametrize("mode", ["pcr", "shift", "identity", "lpa", "uir", "pcr_right"])
 def test_fused_modes(mode):
     w = workloads.make(3, "small")
     _say(f"fused: workload 3 small, mode {mode}")

@@ -28,7 +28,7 @@ pytestmark = pytest.mark.gpu
 MAPS = {64: [((8, 12, 12), False), ((11, 11, 10), True), ((32, 0, 0), False)],
         128: [((16, 24, 24), False), ((22, 21, 21), True), ((24, 20, 20), True),
               ((64, 0, 0), False), ((64, 0, 0), True)]}
-MODES = ["pcr", "shift", "identity", "lpa", "uir"]
+MODES = ["pcr", "shift", "identity", "lpa", "uir", "pcr_right"]
 
 
 def _draw(seed):

@@ -63,7 +63,7 @@ def test_single_token_sits_at_interval_centre():
 
 
 def test_empty_selection():
-    for mode in ("pcr", "shift", "identity", "uir"):
+    for mode in ("pcr", "shift", "identity", "uir", "pcr_right"):
         pos, nxt = reassign(np.zeros((0, 3), int), 77, mode)
         assert pos.shape == (0, 3) and nxt == 78
     assert reassign(np.zeros((0, 3), int), 77, "lpa")[1] == 78
@@ -128,3 +128,35 @@ def test_batch_flags_and_skips_bad_indices():
     # the valid tokens of sequence 0 span h = 0..3 with K = 3
     assert new_pos[0, 1] == float(8 + Fraction(3, 4)) and new_pos[2, 1] == float(8 + Fraction(9, 4))
     assert nxt.tolist() == [11, 21]
+
+
+@settings(max_examples=100, deadline=None)
+@given(pts=st.lists(st.tuples(coord, coord, coord), min_size=1, max_size=30),
+       p_txt=st.integers(min_value=0, max_value=200_000), L=st.integers(min_value=0, max_value=8))
+def test_rightward_pcr_is_leftward_moved_past_the_next_text_position(pts, p_txt, L):
+    """Reading R6: rightward re-anchoring puts the same relative layout in
+    (p_txt + 1, p_txt + L + 2).  In exact arithmetic every coordinate is the
+    leftward one plus L + 1.  The text position is not moved, so the entries sit
+    on future text positions, which is the competition the ablation describes."""
+    c = np.array(pts, dtype=np.int64)
+    left, nl = reassign(c, p_txt, "pcr", L)
+    right, nr = reassign(c, p_txt, "pcr_right", L)
+    assert nl == nr == p_txt + 1
+    assert (right > p_txt + 1).all() and (right < p_txt + L + 2).all()
+    # each side is the correctly rounded double of its rational: compare in Fractions
+    for j in range(len(c)):
+        for a in range(3):
+            assert Fraction(right[j, a]) - Fraction(left[j, a]) == pytest.approx(L + 1, abs=1e-9)
+
+
+def test_rightward_pcr_worked_example_tiny_workload():
+    # p_txt = 299, L = 2, K = 36: the interval starts at 300 instead of 297, so
+    #   p = 300 + 3 (1 + 35 n / 5) / 37 = (11103 + 21 n) / 37,  n = 0..5; t at 301.5
+    pos, nxt = reassign(_c1_coords(), 299, "pcr_right", 2)
+    assert nxt == 300
+    c = _c1_coords()
+    vals = [float(Fraction(11103 + 21 * n, 37)) for n in range(6)]
+    for j in range(36):
+        assert pos[j, 0] == 301.5
+        assert pos[j, 1] == vals[c[j, 1] - 5]
+        assert pos[j, 2] == vals[c[j, 2] - 3]
