@@ -250,3 +250,19 @@ def test_table3_flop_accounting():
     for _, K, printed, hidden, layers in rows:
         val = 3 * int(hidden) * int(layers) * int(K)
         assert f"{val / 1e6:.2f}M" == printed
+
+
+def test_table3_extra_memory_is_768_visual_tokens_of_raw_k_and_v():
+    """Table 3's extra memory (108 MB, 192 MB) is, for both models, exactly the raw K and
+    V memory of 768 visual tokens in bf16 at their cache shapes (Eq. (7), reading R14).
+    The small-K workloads at Table 3's operating points take 768 visual tokens for that
+    reason: their memory must come out at the printed sizes."""
+    import workloads
+    path = os.path.join(os.path.dirname(__file__), "golden", "table3_memory.txt")
+    rows = [l.split() for l in open(path) if l.strip() and not l.startswith("#")]
+    assert len(rows) == 2
+    for model, printed in rows:
+        w = workloads.paper_k(model.lower(), 32)
+        nbytes = int(np.prod(workloads.mem_shape(w))) * 2 * 2      # K and V, bf16
+        assert nbytes == int(printed) * 2 ** 20, (model, nbytes)
+        assert w.M_max == 768
