@@ -384,6 +384,10 @@ prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache
   p.block_size = cache->block_size;
   p.max_blocks = cache->max_blocks;
   p.n_blocks = cache->n_blocks;
+  p.block_shift = -1;
+  if (cache->paged && (cache->block_size & (cache->block_size - 1)) == 0)
+    for (int sh = 0; sh < 31; ++sh)
+      if ((1 << sh) == cache->block_size) p.block_shift = sh;
   p.n_split = n_split;
   p.scale = scale;
   for (int i = 0; i < rope->head_dim / 2; ++i)

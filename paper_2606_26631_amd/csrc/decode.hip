@@ -173,13 +173,17 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
       if (lv[u]) {
         int64_t row;
         if constexpr (kPaged) {
-          const int64_t blk = p.block_table[static_cast<int64_t>(b) * p.max_blocks + j / p.block_size];
+          // Block and offset of slot j: a shift and a mask for power-of-two block
+          // sizes (the common case), else one integer division.
+          const int lb = p.block_shift >= 0 ? (j >> p.block_shift) : j / p.block_size;
+          const int in = j - lb * p.block_size;
+          const int64_t blk = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
           if (blk < 0 || blk >= p.n_blocks) {
             lv[u] = false;
             bad_block = 1;
             continue;
           }
-          row = ((static_cast<int64_t>(p.layer) * p.n_blocks + blk) * p.block_size + j % p.block_size) *
+          row = ((static_cast<int64_t>(p.layer) * p.n_blocks + blk) * p.block_size + in) *
                     p.n_kv_heads + kvh;
         } else {
           row = row_base + j;

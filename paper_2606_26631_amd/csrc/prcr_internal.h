@@ -122,6 +122,7 @@ struct DecodeParams {
   int32_t *err;
   int32_t batch, n_layers, n_kv_heads, n_q_heads, layer;
   int32_t s_max, block_size, max_blocks, n_blocks;
+  int32_t block_shift;            // log2(block_size) if a power of two, else -1
   int32_t n_split;                // workgroups per (sequence, KV head)
   float scale;
   double inv_freq[kMaxPairs];
