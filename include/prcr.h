@@ -22,8 +22,10 @@
  *     between calls and allocates no memory; calls are re-entrant.
  *   - Structural errors (null pointer, bad shape, misalignment, unsupported
  *     combination) are detected on the host before any HIP call and returned;
- *     nothing is launched and no output is touched.  A failed kernel launch
- *     returns PRCR_ERR_HIP.
+ *     nothing is launched and no output is touched.  A problem too large for
+ *     one launch (a grid dimension beyond 2^32 - 1 work-items, which the dispatch
+ *     cannot express) is such an error too: PRCR_ERR_SHAPE.  A failed kernel
+ *     launch returns PRCR_ERR_HIP.
  *   - Data errors found on the device (an index outside the visual-token range,
  *     a slot beyond the cache capacity, a block-table entry outside the pool,
  *     malformed selection offsets, a position outside the exact range) OR their

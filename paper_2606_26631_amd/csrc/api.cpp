@@ -11,11 +11,18 @@ using namespace prcr;
 
 namespace {
 
-constexpr int32_t kVersion = 1 * 10000 + 3 * 100 + 0;
+constexpr int32_t kVersion = 1 * 10000 + 3 * 100 + 1;
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 int elem_bytes(prcr_dtype d) { return d == PRCR_F32 ? 4 : 2; }
+
+// A launcher's own refusal of a grid too large for one dispatch is a size error
+// found before any HIP call; anything else the runtime reports is a launch error.
+prcr_status launch_status(hipError_t e) {
+  if (e == hipSuccess) return PRCR_OK;
+  return e == hipErrorInvalidConfiguration ? PRCR_ERR_SHAPE : PRCR_ERR_HIP;
+}
 
 prcr_status check_rope(const prcr_rope *rope) {
   if (rope == nullptr) return PRCR_ERR_NULL;
@@ -143,7 +150,7 @@ prcr_status prcr_store_raw(const prcr_mem *mem, int32_t layer, const void *raw_k
   p.layer = layer;
   p.s_src = s_src;
   p.row_bytes = mem->n_kv_heads * mem->head_dim * elem_bytes(mem->dtype);
-  return launch_store(p, stream) == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
+  return launch_status(launch_store(p, stream));
 }
 
 prcr_status prcr_reassign_coords(const prcr_mem *mem, const int32_t *sel_off, const int32_t *sel_idx,
@@ -174,7 +181,7 @@ prcr_status prcr_reassign_coords(const prcr_mem *mem, const int32_t *sel_off, co
   p.total_k = total_k;
   p.mode = static_cast<int32_t>(mode);
   p.l_ext = l_ext;
-  return launch_reassign(p, stream) == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
+  return launch_status(launch_reassign(p, stream));
 }
 
 }  // extern "C"
@@ -252,7 +259,7 @@ prcr_status prcr_rebind_inject(const prcr_rope *rope, const prcr_mem *mem, const
   if (new_pos != nullptr && !aligned(new_pos, 8)) return PRCR_ERR_ALIGN;
   p.new_pos = new_pos;
   const hipError_t e = launch_rebind(p, mem->dtype, mem->head_dim, map, cache->paged != 0, false, stream);
-  return e == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
+  return launch_status(e);
 }
 
 prcr_status prcr_prefill_capture(const prcr_rope *rope, const prcr_mem *mem, int32_t layer,
@@ -308,7 +315,7 @@ prcr_status prcr_prefill_capture(const prcr_rope *rope, const prcr_mem *mem, int
   for (int i = 0; i < rope->head_dim / 2; ++i)
     p.inv_freq[i] = std::pow(rope->theta, -(2.0 * i) / rope->head_dim);
   const hipError_t e = launch_prefill(p, mem->dtype, mem->head_dim, map, cache->paged != 0, stream);
-  return e == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
+  return launch_status(e);
 }
 
 static prcr_status decode_shape(const prcr_cache *cache, int32_t batch, int32_t n_q_heads,
@@ -393,7 +400,7 @@ prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache
   for (int i = 0; i < rope->head_dim / 2; ++i)
     p.inv_freq[i] = std::pow(rope->theta, -(2.0 * i) / rope->head_dim);
   const hipError_t e = launch_decode(p, dtype, rope->head_dim, cache->paged != 0, stream);
-  return e == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
+  return launch_status(e);
 }
 
 prcr_status prcr_revisit(const prcr_rope *rope, const prcr_mem *mem, const int32_t *sel_off,
@@ -418,7 +425,7 @@ prcr_status prcr_revisit(const prcr_rope *rope, const prcr_mem *mem, const int32
   p.mode = static_cast<int32_t>(mode);
   p.l_ext = l_ext;
   const hipError_t e = launch_rebind(p, mem->dtype, mem->head_dim, map, cache->paged != 0, true, stream);
-  return e == hipSuccess ? PRCR_OK : PRCR_ERR_HIP;
+  return launch_status(e);
 }
 
 }  // extern "C"

@@ -141,6 +141,13 @@ enum class AxisMapId : int {
 };
 
 AxisMapId axis_map_id(const prcr_rope &rope);
+
+// The dispatch packet holds each grid dimension as a 32-bit count of work-items:
+// a launcher refuses (hipErrorInvalidConfiguration, before any HIP call) a grid
+// whose x extent would not fit.
+inline bool grid_fits(int64_t blocks, int threads) {
+  return blocks >= 1 && blocks <= static_cast<int64_t>(UINT32_MAX) / threads;
+}
 int axis_of_pair(AxisMapId id, int i);
 
 // Launchers (return the hipError_t of the launch).

@@ -176,7 +176,7 @@ hipError_t launch_one(const PrefillParams &p, hipStream_t stream) {
   const int64_t per_block = static_cast<int64_t>(kWaves) * RPI * kIters;
   int64_t blocks = (rows_all + per_block - 1) / per_block;
   if (blocks < 1) blocks = 1;
-  if (blocks > INT32_MAX) return hipErrorInvalidConfiguration;
+  if (!grid_fits(blocks, kWaves * kWave)) return hipErrorInvalidConfiguration;
   prefill_capture_kernel<T, D, Map, kPaged><<<dim3(static_cast<unsigned>(blocks)), kWaves * kWave, 0,
                                               stream>>>(p);
   return hipGetLastError();

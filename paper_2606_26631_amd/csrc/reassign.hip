@@ -127,6 +127,7 @@ __global__ __launch_bounds__(kThreads) void reassign_kernel(const ReassignParams
 }  // namespace
 
 hipError_t launch_reassign(const ReassignParams &p, hipStream_t stream) {
+  if (!grid_fits(p.batch, kThreads)) return hipErrorInvalidConfiguration;
   reassign_kernel<<<dim3(p.batch), dim3(kThreads), 0, stream>>>(p);
   return hipGetLastError();
 }

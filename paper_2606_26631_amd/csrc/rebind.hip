@@ -385,7 +385,7 @@ hipError_t launch_one(const RebindParams &in, hipStream_t stream) {
   const int64_t n_tblk = (static_cast<int64_t>(p.total_k) + kWavesPerBlock - 1) / kWavesPerBlock;
   int64_t n_work = n_tblk * p.n_row_groups * 2;
   if (n_work < 1) n_work = 1;
-  if (n_work > INT32_MAX) return hipErrorInvalidConfiguration;
+  if (!grid_fits(n_work, kWavesPerBlock * kWave)) return hipErrorInvalidConfiguration;
   const dim3 grid(static_cast<unsigned>(n_work));
   rebind_inject_kernel<T, D, Map, kPaged, kWavesPerBlock, kUnrollRows, kFused>
       <<<grid, kWavesPerBlock * kWave, 0, stream>>>(p);

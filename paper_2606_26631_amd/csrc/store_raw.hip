@@ -56,7 +56,9 @@ __global__ __launch_bounds__(kWaves * kWave) void store_raw_kernel(const StorePa
 }  // namespace
 
 hipError_t launch_store(const StoreParams &p, hipStream_t stream) {
-  const dim3 grid((p.max_visual + kWaves - 1) / kWaves, p.batch);
+  const int64_t blocks = (static_cast<int64_t>(p.max_visual) + kWaves - 1) / kWaves;
+  if (!grid_fits(blocks, kWaves * kWave)) return hipErrorInvalidConfiguration;
+  const dim3 grid(static_cast<unsigned>(blocks), p.batch);
   store_raw_kernel<<<grid, kWaves * kWave, 0, stream>>>(p);
   return hipGetLastError();
 }

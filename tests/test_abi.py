@@ -41,7 +41,7 @@ def test_library_exports_every_declared_function():
     assert {"prcr_store_raw", "prcr_reassign_coords", "prcr_rebind_inject"} <= set(names)
     for n in names:
         assert hasattr(L, n), f"{n} declared in prcr.h but not exported"
-    assert L.prcr_version() == 10300
+    assert L.prcr_version() == 10301
 
 
 def test_status_strings():
@@ -198,6 +198,20 @@ def test_revisit_validation_errors():
     assert call_revisit(r2, m2, c2) == 1
     r2, m2, c2 = good(); r2.section[0], r2.section[1] = 32, 8
     assert call_revisit(r2, m2, c2) == 6
+
+
+@host_only
+def test_grid_limits():
+    # A launch carries each grid extent as a 32-bit count of work-items (256 per
+    # workgroup here).  Problems beyond it are size errors, refused before any HIP
+    # call, so these placeholder pointers are never used.
+    rope, mem, cache = good()
+    assert call_rebind(rope, mem, cache, total_k=1 << 25) == 2
+    r2, m2, c2 = good(); m2.batch = 1 << 24                # one workgroup per sequence
+    assert call_reassign(m2) == 2
+    r2, m2, c2 = good(); m2.max_visual = 1 << 26           # four tokens per workgroup
+    assert call_store(m2) == 2
+    assert call_prefill(rope, mem, cache, s_src=1 << 27) == 2
 
 
 def call_prefill(rope, mem, cache, layer=0, raw_k=FAKE, raw_v=FAKE, s_src=10, pos=FAKE,
