@@ -299,7 +299,9 @@ prcr_status prcr_revisit(const prcr_rope *rope, const prcr_mem *mem,
  * Scores and the softmax are accumulated in float32; the query is rotated in
  * double and rounded to float32 once.  cache_len[b] = 0 gives out = 0.  A
  * cache_len beyond the capacity is clamped with PRCR_DERR_CAPACITY; a block-table
- * entry outside the pool skips its keys with PRCR_DERR_BLOCK.
+ * entry outside the pool skips its keys with PRCR_DERR_BLOCK.  The capacity per
+ * sequence (s_max, or max_blocks * block_size) is at most 2^30 slots, else
+ * PRCR_ERR_SHAPE.
  */
 prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache,
                                   prcr_dtype dtype, int32_t batch, int32_t n_layers,

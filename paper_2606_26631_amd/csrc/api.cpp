@@ -12,6 +12,7 @@ using namespace prcr;
 namespace {
 
 constexpr int32_t kVersion = 1 * 10000 + 3 * 100 + 1;
+constexpr int64_t kMaxDecodeSlots = int64_t{1} << 30;   // decode: cache capacity per sequence
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -334,7 +335,8 @@ static prcr_status decode_shape(const prcr_cache *cache, int32_t batch, int32_t 
     if (cache->s_max < 1) return PRCR_ERR_SHAPE;
     cap = cache->s_max;
   }
-  if (cap > INT32_MAX) return PRCR_ERR_SHAPE;
+  // Slot indices, plus a few batches of look-ahead, stay far inside 32 bits.
+  if (cap > kMaxDecodeSlots) return PRCR_ERR_SHAPE;
   *n_split = decode_splits(cap, batch, n_kv_heads);
   return PRCR_OK;
 }

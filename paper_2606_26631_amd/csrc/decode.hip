@@ -161,36 +161,48 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
   // scored, so one batch is always in flight.
   u32x4 kc[kIters], vc[kIters];
   bool live[kIters];
+  // Slot 0 of this head's first row of the layer: present in every cache.
+  const int64_t row_any = kPaged ? static_cast<int64_t>(p.layer) * p.n_blocks * p.block_size * p.n_kv_heads + kvh
+                                 : row_base;
   auto load_batch = [&](int jb, u32x4 *kd, u32x4 *vd, bool *lv) {
+    int32_t blk[kIters], in[kIters];
+    if constexpr (kPaged) {
+      // Every block-table entry of the batch is read before any row load is
+      // issued: a wait for a table entry also waits for every load issued before
+      // it, so reading them row by row would serialise the batch's row loads.
+      // Rows past the chunk read the sequence's first entry (always present).
+#pragma unroll
+      for (int u = 0; u < kIters; ++u) {
+        const int j = jb + u * KPB + grp;
+        const int js = j < j1 ? j : 0;
+        // Block and offset of slot js: a shift and a mask for power-of-two block
+        // sizes (the common case), else one integer division.
+        const int lb = p.block_shift >= 0 ? (js >> p.block_shift) : js / p.block_size;
+        in[u] = js - lb * p.block_size;
+        blk[u] = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
+      }
+    }
 #pragma unroll
     for (int u = 0; u < kIters; ++u) {
       const int j = jb + u * KPB + grp;
       lv[u] = j < j1;
-      // Rows past the chunk stay zero: the update below is branch-free and a
-      // zero weight times a stale register could otherwise make a NaN.
-      kd[u] = u32x4{0u, 0u, 0u, 0u};
-      vd[u] = u32x4{0u, 0u, 0u, 0u};
-      if (lv[u]) {
-        int64_t row;
-        if constexpr (kPaged) {
-          // Block and offset of slot j: a shift and a mask for power-of-two block
-          // sizes (the common case), else one integer division.
-          const int lb = p.block_shift >= 0 ? (j >> p.block_shift) : j / p.block_size;
-          const int in = j - lb * p.block_size;
-          const int64_t blk = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
-          if (blk < 0 || blk >= p.n_blocks) {
-            lv[u] = false;
-            bad_block = 1;
-            continue;
-          }
-          row = ((static_cast<int64_t>(p.layer) * p.n_blocks + blk) * p.block_size + in) *
-                    p.n_kv_heads + kvh;
-        } else {
-          row = row_base + j;
+      int64_t row;
+      if constexpr (kPaged) {
+        if (lv[u] && (blk[u] < 0 || blk[u] >= p.n_blocks)) {
+          lv[u] = false;
+          bad_block = 1;
         }
-        kd[u] = load_nt(static_cast<const char *>(p.cache_k) + row * kRowBytes + c * 16);
-        vd[u] = load_nt(static_cast<const char *>(p.cache_v) + row * kRowBytes + c * 16);
+        row = ((static_cast<int64_t>(p.layer) * p.n_blocks + blk[u]) * p.block_size + in[u]) *
+                  p.n_kv_heads + kvh;
+      } else {
+        row = row_base + j;
       }
+      // Rows past the chunk (or in a block outside the pool) read a row that
+      // always exists, so that every load is issued unconditionally; they get
+      // zero weight, and their values are taken as zero when scored.
+      row = lv[u] ? row : row_any;
+      kd[u] = load_nt(static_cast<const char *>(p.cache_k) + row * kRowBytes + c * 16);
+      vd[u] = load_nt(static_cast<const char *>(p.cache_v) + row * kRowBytes + c * 16);
     }
   };
   load_batch(j0, kc, vc, live);
@@ -213,9 +225,11 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
         sc[u][g] = group_sum<LPK>(s);
       }
     }
+    // A zero weight times a value read from another row could make a NaN:
+    // values of rows without weight are taken as zero.
     float v[kIters][EPL];
 #pragma unroll
-    for (int u = 0; u < kIters; ++u) Elems<T>::unpack(vc[u], v[u]);
+    for (int u = 0; u < kIters; ++u) Elems<T>::unpack(live[u] ? vc[u] : u32x4{0u, 0u, 0u, 0u}, v[u]);
 #pragma unroll
     for (int g = 0; g < GT; ++g) {
       float mn = m[g];

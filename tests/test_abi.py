@@ -282,6 +282,11 @@ def test_decode_validation_errors():
     assert call_decode(r2, c2) == 2                         # paged with zero sizes
     r2, _, c2 = good(); c2.paged, c2.block_size, c2.max_blocks, c2.n_blocks = 1, 16, 4, 8
     assert call_decode(r2, c2) == 1                         # paged without a block table
+    r2, _, c2 = good(); c2.s_max = (1 << 30) + 1
+    assert call_decode(r2, c2) == 2                         # capacity above 2^30 slots
+    r2, _, c2 = good(); c2.paged, c2.block_table = 1, FAKE
+    c2.block_size, c2.max_blocks, c2.n_blocks = 1 << 16, (1 << 14) + 1, 8
+    assert call_decode(r2, c2) == 2
 
 
 def test_decode_workspace_size():
