@@ -207,3 +207,81 @@ def test_decode_many_sequences():
     ref = oracle.decode_attention(rope.__dict__ | {"sections": rope.sections}, cache_o, layer,
                                   q.numpy(), q_pos, lens, D ** -0.5, "f32")
     _check(out, ref, cache_o, lens, H, G, "f32", layer)
+
+
+def _reference_over_kept(rope_d, cache_o, layer, q, q_pos, lens_eff, skip, dtype):
+    """The oracle's attention over the keys the library keeps: slots below
+    lens_eff[b], minus the logical blocks skip[b].  Attention does not depend on
+    the order of its keys, so the kept rows of each sequence are packed into a
+    contiguous cache and handed to the oracle unchanged."""
+    kk, vv = cache_o["k"], cache_o["v"]
+    paged = cache_o["paged"]
+    NL, H, D = (kk.shape[0], kk.shape[3], kk.shape[4]) if paged else (kk.shape[1], kk.shape[2], kk.shape[4])
+    bs = cache_o.get("block_size", 1)
+    keep = [[s for s in range(int(n)) if not (paged and s // bs in skip.get(b, ()))]
+            for b, n in enumerate(lens_eff)]
+    cap = max(1, max(len(x) for x in keep))
+    kc = np.zeros((len(keep), NL, H, cap, D), kk.dtype)
+    vc = np.zeros_like(kc)
+    for b, slots in enumerate(keep):
+        for i, s in enumerate(slots):
+            if paged:
+                blk = cache_o["block_table"][b, s // bs]
+                kc[b, layer, :, i], vc[b, layer, :, i] = kk[layer, blk, s % bs], vv[layer, blk, s % bs]
+            else:
+                kc[b, layer, :, i], vc[b, layer, :, i] = kk[b, layer, :, s], vv[b, layer, :, s]
+    packed = {"paged": False, "s_max": cap, "k": kc, "v": vc}
+    kept = np.array([len(x) for x in keep], np.int32)
+    ref = oracle.decode_attention(rope_d, packed, layer, q, q_pos, kept, D ** -0.5, dtype)
+    return ref, packed, kept
+
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_decode_data_errors(paged):
+    """Data errors of decode attention, as the header documents them: a cache_len
+    below 0 or above the capacity is clamped (PRCR_DERR_CAPACITY), and a block-table
+    entry outside the pool skips that block's keys (PRCR_DERR_BLOCK).  The output is
+    the oracle's attention over the keys that remain.  Paged: pool block 0 holds NaN
+    in every layer and no table entry names it, so a skipped or past-the-end row
+    whose value leaked into a sum would show as NaN."""
+    B, NL, H, D, G, layer = 4, 2, 2, 128, 4, 1
+    g = torch.Generator().manual_seed(501)
+    rnd = lambda *s: torch.randn(s, generator=g).to(torch.bfloat16)
+    rng = np.random.default_rng(502)
+    if paged:
+        bs, need = 16, 40
+        cap, n_blocks = bs * need, B * need + 1
+        table = (1 + rng.permutation(B * need)).astype(np.int32).reshape(B, need)
+        table[0, 3] = -1                    # slots 48..63 of sequence 0
+        table[1, 0] = n_blocks + 7          # slots 0..15 of sequence 1
+        table[3, need - 1] = n_blocks       # the last block of sequence 3
+        skip = {0: {3}, 1: {0}, 3: {need - 1}}
+        k, v = rnd(NL, n_blocks, bs, H, D), rnd(NL, n_blocks, bs, H, D)
+        k[:, 0], v[:, 0] = float("nan"), float("nan")
+        lens = np.array([500, 333, cap + 40, cap], np.int32)
+        expect = prcr.DERR_BLOCK | prcr.DERR_CAPACITY
+        cache_o = {"paged": True, "block_size": bs, "block_table": table, "max_blocks": need,
+                   "n_blocks": n_blocks}
+        cache = prcr.Cache(k.to(DEV), v.to(DEV), to_dev(table))
+    else:
+        cap = 600
+        skip = {}
+        k, v = rnd(B, NL, H, cap, D), rnd(B, NL, H, cap, D)
+        lens = np.array([-3, cap + 9, 100, 0], np.int32)
+        expect = prcr.DERR_CAPACITY
+        cache_o = {"paged": False, "s_max": cap}
+        cache = prcr.Cache(k.to(DEV), v.to(DEV))
+    cache_o["k"], cache_o["v"] = workloads.as_numpy_storage(k), workloads.as_numpy_storage(v)
+    q = rnd(B, H * G, D)
+    q_pos = rng.integers(0, 20000, B).astype(np.int32)
+    rope = prcr.Rope(D, (16, 24, 24), False, 1e6)
+    _say(f"decode attention data errors, paged={paged}, lens {lens.tolist()}")
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out = prcr.decode_attention(rope, cache, layer, q.to(DEV), to_dev(q_pos), to_dev(lens), err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == expect
+    assert torch.isfinite(out).all()
+    ref, packed, kept = _reference_over_kept(rope.__dict__ | {"sections": rope.sections}, cache_o,
+                                             layer, workloads.as_numpy_storage(q), q_pos,
+                                             np.clip(lens, 0, cap), skip, "bf16")
+    _check(out, ref, packed, kept, H, G, "bf16", layer)
