@@ -10,6 +10,7 @@
 // data moves between lanes in the hot loop.  K and V rows are read and written
 // with 16-byte non-temporal accesses: every byte is touched exactly once.
 #include <cmath>
+#include <type_traits>
 
 #include "positions.h"
 #include "prcr_internal.h"
@@ -41,6 +42,13 @@ __device__ __forceinline__ u32x4 load16(const char *p) {
   return *reinterpret_cast<const u32x4 *>(p);
 #endif
 }
+// Logical block of a non-negative slot: one 32-bit division for slots below
+// 2^31 (every real cache), the 64-bit one beyond.
+__device__ __forceinline__ int64_t block_of(int64_t slot, int32_t block_size) {
+  if (slot <= INT32_MAX)
+    return static_cast<int64_t>(static_cast<uint32_t>(slot) / static_cast<uint32_t>(block_size));
+  return slot / block_size;
+}
 __device__ __forceinline__ void store16(char *p, u32x4 v) {
 #if PRCR_NONTEMPORAL
   store_nt(p, v);
@@ -56,10 +64,14 @@ __device__ __forceinline__ void store16(char *p, u32x4 v) {
 // each wave streams one source and one destination (faster than moving both
 // arrays in one wave).
 //
-// Latency: the wave issues the loads of its first rows as soon as the source row
-// is known to be in range, before the remaining validation, position and cos/sin
-// work, and afterwards always loads the next batch of rows while it stores the
-// current one.
+// Latency.  Vector loads complete in issue order, and a wait for one load also
+// waits for every load issued before it, so the wave issues its loads in as few
+// dependent rounds as the data allows: (1) its token index, (2) the first rows
+// (once the source row is known to be in range) together with every
+// per-sequence value, from clamped indices and without branches, and (3) in
+// the fused kernel, the coordinates of the sequence's first 64 selected tokens
+// (paged: with the destination block-table entry).  Afterwards it always has
+// the next batch of rows in flight while it stores the current one.
 //
 // Key-only memory (v_slot set, no memory values): value waves copy the rows of
 // cache slot v_slot[b][m] of the same sequence, which lies below cache_len[b]
@@ -117,68 +129,115 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
   const int row0 = grp * p.rows_per_wave;
   const int row_end = min(rows_total, row0 + p.rows_per_wave);
 
-  // Loads that depend only on g are issued first ...
-  const int m = p.sel_idx[g];
-  double pt = 0.0, ph = 0.0, pw = 0.0;
-  if (!kFused && keys) {
-    pt = p.new_pos[3 * static_cast<int64_t>(g) + 0];
-    ph = p.new_pos[3 * static_cast<int64_t>(g) + 1];
-    pw = p.new_pos[3 * static_cast<int64_t>(g) + 2];
-  }
-  // ... then the sequence of g: (number of offsets <= g) - 1, by a ballot over
-  // the offsets held one per lane ...
-  int cnt = 0;
-  for (int base = 0; base <= p.batch; base += kWave) {
-    const int i = base + lane;
-    const bool le = (i <= p.batch) && (p.sel_off[i] <= g);
-    cnt += __popcll(__ballot(le));
-  }
-  const int b = __builtin_amdgcn_readfirstlane(cnt - 1);
+  // The key and value halves of the grid run separate copies of the code below
+  // (keys is uniform across the workgroup), so that each half compiles to
+  // straight-line loads with no branch on the half between a load and its use.
+  auto half = [&](auto key_half) {
+    constexpr bool keys = decltype(key_half)::value;
+    // Loads that depend only on g are issued first ...
+    const int m = p.sel_idx[g];
+    double pt = 0.0, ph = 0.0, pw = 0.0;
+    if (!kFused && keys) {
+      pt = p.new_pos[3 * static_cast<int64_t>(g) + 0];
+      ph = p.new_pos[3 * static_cast<int64_t>(g) + 1];
+      pw = p.new_pos[3 * static_cast<int64_t>(g) + 2];
+    }
+    // ... then the sequence of g: (number of offsets <= g) - 1, by a ballot over
+    // the offsets held one per lane.  With fewer than 64 sequences one pass holds
+    // every offset, and the sequence's own two are read from lanes b and b + 1.
+    int cnt = 0, off_lane = 0;
+    for (int base = 0; base <= p.batch; base += kWave) {
+      const int i = base + lane;
+      off_lane = i <= p.batch ? p.sel_off[i] : INT_MAX;
+      cnt += __popcll(__ballot(off_lane <= g));
+    }
+    const int b = __builtin_amdgcn_readfirstlane(cnt - 1);
+    const int bq = min(max(b, 0), p.batch - 1);
+    int s0, s1;
+    if (p.batch < kWave) {
+      s0 = __builtin_amdgcn_readfirstlane(__shfl(off_lane, bq));
+      s1 = __builtin_amdgcn_readfirstlane(__shfl(off_lane, bq + 1));
+    } else {
+      s0 = p.sel_off[bq];
+      s1 = p.sel_off[bq + 1];
+    }
+    const bool offsets_ok = b >= 0 && b < p.batch && s0 >= 0 && s0 <= g && g < s1 && s1 <= p.total_k;
 
-  // The source rows exist whenever b and m are in range: start loading them
-  // (memory rows; cache rows of a key-only memory are loaded after validation).
-  const bool alias_v = !keys && p.v_slot != nullptr;
-  const bool src_ok = b >= 0 && b < p.batch && m >= 0 && m < p.max_visual;
-  const size_t tok_off = src_ok ? (static_cast<size_t>(b) * p.max_visual + m) * rows_total : 0;
-  const char *src = static_cast<const char *>(keys ? p.mem_k : (alias_v ? p.cache_v : p.mem_v)) +
-                    (alias_v ? 0 : tok_off * kRowBytes) + c * 16;
-  char *dst = static_cast<char *>(keys ? p.cache_k : p.cache_v) + c * 16;
-  u32x4 lo[kUnroll], hi[kUnroll];
-  if (!alias_v) {
+    // The source rows exist whenever b and m are in range: start loading them
+    // (memory rows; cache rows of a key-only memory are loaded after validation).
+    const bool alias_v = !keys && p.v_slot != nullptr;
+    const bool src_ok = b >= 0 && b < p.batch && m >= 0 && m < p.max_visual;
+    const size_t tok_off = src_ok ? (static_cast<size_t>(b) * p.max_visual + m) * rows_total : 0;
+    const char *src = static_cast<const char *>(keys ? p.mem_k : (alias_v ? p.cache_v : p.mem_v)) +
+                      (alias_v ? 0 : tok_off * kRowBytes) + c * 16;
+    char *dst = static_cast<char *>(keys ? p.cache_k : p.cache_v) + c * 16;
+    u32x4 lo[kUnroll], hi[kUnroll];
+    if (!alias_v) {
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int row = row0 + u * RPI + r;
-      if (src_ok && row < row_end) {
-        lo[u] = load16(src + static_cast<size_t>(row) * kRowBytes);
-        hi[u] = load16(src + static_cast<size_t>(row) * kRowBytes + kHalfBytes);
+      for (int u = 0; u < kUnroll; ++u) {
+        const int row = row0 + u * RPI + r;
+        if (src_ok && row < row_end) {
+          lo[u] = load16(src + static_cast<size_t>(row) * kRowBytes);
+          hi[u] = load16(src + static_cast<size_t>(row) * kRowBytes + kHalfBytes);
+        }
       }
     }
-  }
 
-  // Per-sequence values, all at once from a clamped index, and validation.
-  const int bq = min(max(b, 0), p.batch - 1);
-  const int s0 = p.sel_off[bq];
-  const int s1 = p.sel_off[bq + 1];
-  const int nvis = p.n_visual[bq];
-  const int64_t slot = static_cast<int64_t>(p.cache_len[bq]) + (g - s0);
+    // Every per-sequence value is loaded in the same round trip as the rows, from
+    // clamped indices (always inside the arrays) and without branches, so that no
+    // load waits on another.  The fused kernel also loads the text position, this
+    // token's coordinates and the sequence's first 64 selected indices (Eq. (8)).
+    const int nvis = p.n_visual[bq];
+    const int64_t clen = p.cache_len[bq];
+    const int K = s1 - s0;
+    int64_t ptxt = 0;
+    int cm0 = 0, cm1 = 0, cm2 = 0, mj0 = -1;
+    if constexpr (kFused && keys) {
+      ptxt = p.p_txt[bq];
+      const int mc = min(max(m, 0), p.max_visual - 1);
+      const int32_t *cm = p.coords + (static_cast<int64_t>(bq) * p.max_visual + mc) * 3;
+      cm0 = cm[0];
+      cm1 = cm[1];
+      cm2 = cm[2];
+      mj0 = p.sel_idx[min(max(s0 + lane, 0), p.total_k - 1)];
+    }
 
-  int flags = 0;
-  const bool offsets_ok = b >= 0 && b < p.batch && s0 <= g && g < s1;
-  bool ok = offsets_ok;
-  if (!ok) {
-    flags = PRCR_DERR_OFFSETS;
-  } else if (m < 0 || m >= nvis || m >= p.max_visual) {
-    ok = false;
-    flags = PRCR_DERR_INDEX;
-  }
-  if constexpr (kFused) {
-    if (keys && offsets_ok) {
-      // Eq. (8): ranges of the sequence's valid selected coordinates.
-      const int K = s1 - s0;
+    // Validation, without branches: a value used only inside a branch could have
+    // its load moved into that branch, a round trip later.
+    const int64_t slot = clen + (g - s0);
+    const bool index_ok = m >= 0 && m < nvis && m < p.max_visual;
+    bool ok = offsets_ok && index_ok;
+    int flags = !offsets_ok ? PRCR_DERR_OFFSETS : (index_ok ? 0 : PRCR_DERR_INDEX);
+    // Destination slot.  Paged: its block-table entry is read at once, from a
+    // clamped logical block (always inside the table); a block beyond the table
+    // is flagged below.
+    int64_t slot_id = -1, blk = 0, off = 0;
+    int slot_flag = 0;
+    if constexpr (kPaged) {
+      const int64_t lb = slot >= 0 ? block_of(slot, p.block_size) : -1;
+      const int64_t lbc = min(max(lb, int64_t{0}), static_cast<int64_t>(p.max_blocks) - 1);
+      blk = p.block_table[static_cast<int64_t>(bq) * p.max_blocks + lbc];
+      off = slot - lb * p.block_size;
+      if (lb < 0 || lb >= p.max_blocks) slot_flag = PRCR_DERR_CAPACITY;
+    }
+    if constexpr (kFused && keys) {
+      // Eq. (8): ranges of the sequence's valid selected coordinates, over a
+      // well-formed sequence (a malformed one reduces over nothing).
+      // The positions are then formed whatever the validity, so that the values
+      // loaded above are used outside any branch: used only inside one, their
+      // loads could be moved into it, a round trip later.
+      const int Kr = offsets_ok ? K : 0;
       const int lim = min(nvis, p.max_visual);
-      const int32_t *cb = p.coords + static_cast<int64_t>(b) * p.max_visual * 3;
-      int lo0 = INT_MAX, lo1 = INT_MAX, lo2 = INT_MAX, hi0 = INT_MIN, hi1 = INT_MIN, hi2 = INT_MIN;
-      for (int j = lane; j < K; j += kWave) {
+      const int32_t *cb = p.coords + static_cast<int64_t>(bq) * p.max_visual * 3;
+      // The first 64 selected tokens: their coordinates are loaded from a clamped
+      // index on every lane, and an absent or invalid entry is masked out.
+      const int mc0 = min(max(mj0, 0), p.max_visual - 1);
+      const int32_t *cf = cb + 3 * mc0;
+      const int f0 = cf[0], f1 = cf[1], f2 = cf[2];
+      const bool first = lane < Kr && mj0 >= 0 && mj0 < lim;
+      int lo0 = first ? f0 : INT_MAX, lo1 = first ? f1 : INT_MAX, lo2 = first ? f2 : INT_MAX;
+      int hi0 = first ? f0 : INT_MIN, hi1 = first ? f1 : INT_MIN, hi2 = first ? f2 : INT_MIN;
+      for (int j = lane + kWave; j < Kr; j += kWave) {
         const int mj = p.sel_idx[s0 + j];
         if (mj >= 0 && mj < lim) {
           const int c0 = cb[3 * mj], c1 = cb[3 * mj + 1], c2 = cb[3 * mj + 2];
@@ -192,18 +251,15 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
         lo1 = min(lo1, __shfl_xor(lo1, o)); hi1 = max(hi1, __shfl_xor(hi1, o));
         lo2 = min(lo2, __shfl_xor(lo2, o)); hi2 = max(hi2, __shfl_xor(hi2, o));
       }
-      const int64_t ptxt = p.p_txt[b];
+      // Eq. (9)-(10).  Safe on any input (magnitudes are checked before the
+      // integer products); the values only count for a valid token.
       bool range_bad = false;
-      if (ok) {
-        const int32_t *cm = cb + 3 * static_cast<int64_t>(m);
-        const int64_t j = g - s0;
-        pt = reassigned(p.mode, ptxt, p.l_ext, K, j, lo0, hi0, cm[0], &range_bad);
-        ph = reassigned(p.mode, ptxt, p.l_ext, K, j, lo1, hi1, cm[1], &range_bad);
-        pw = reassigned(p.mode, ptxt, p.l_ext, K, j, lo2, hi2, cm[2], &range_bad);
-      } else {
-        pt = ph = pw = __builtin_nan("");
-      }
-      if (grp == 0 && lane == 0) {
+      const int64_t j = static_cast<int64_t>(g) - s0;
+      pt = reassigned(p.mode, ptxt, p.l_ext, K, j, lo0, hi0, cm0, &range_bad);
+      ph = reassigned(p.mode, ptxt, p.l_ext, K, j, lo1, hi1, cm1, &range_bad);
+      pw = reassigned(p.mode, ptxt, p.l_ext, K, j, lo2, hi2, cm2, &range_bad);
+      if (!ok) pt = ph = pw = __builtin_nan("");
+      if (offsets_ok && grp == 0 && lane == 0) {
         if (p.pos_out != nullptr) {
           p.pos_out[3 * static_cast<int64_t>(g) + 0] = pt;
           p.pos_out[3 * static_cast<int64_t>(g) + 1] = ph;
@@ -217,140 +273,145 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
                                          : 0;
           p.next_pos[b] = static_cast<int32_t>(next_text_position(p.mode, ptxt, K, any_valid, span));
         }
-        if (range_bad && p.err != nullptr) atomicOr(p.err, PRCR_DERR_RANGE);
+        if (ok && range_bad && p.err != nullptr) atomicOr(p.err, PRCR_DERR_RANGE);
       }
     }
-  }
-  // Key-only memory: the value slot must be one of the sequence's filled slots.
-  int64_t vslot = 0, vpool = 0;
-  if (ok && p.v_slot != nullptr) {
-    vslot = p.v_slot[static_cast<int64_t>(b) * p.max_visual + m];
-    if (vslot < 0 || vslot >= p.cache_len[b]) {
-      ok = false;
-      flags = PRCR_DERR_INDEX;
-    } else if constexpr (kPaged) {
-      const int64_t lb = vslot / p.block_size;
-      if (lb >= p.max_blocks) {
+    // Key-only memory: the value slot must be one of the sequence's filled slots.
+    int64_t vslot = 0, vpool = 0;
+    if (ok && p.v_slot != nullptr) {
+      vslot = p.v_slot[static_cast<int64_t>(b) * p.max_visual + m];
+      if (vslot < 0 || vslot >= clen) {
         ok = false;
-        flags = PRCR_DERR_CAPACITY;
-      } else {
-        const int64_t vb = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
-        if (vb < 0 || vb >= p.n_blocks) {
+        flags = PRCR_DERR_INDEX;
+      } else if constexpr (kPaged) {
+        const int64_t lb = block_of(vslot, p.block_size);
+        if (lb >= p.max_blocks) {
           ok = false;
-          flags = PRCR_DERR_BLOCK;
+          flags = PRCR_DERR_CAPACITY;
         } else {
-          vpool = vb * p.block_size + (vslot - lb * p.block_size);
+          const int64_t vb = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
+          if (vb < 0 || vb >= p.n_blocks) {
+            ok = false;
+            flags = PRCR_DERR_BLOCK;
+          } else {
+            vpool = vb * p.block_size + (vslot - lb * p.block_size);
+          }
         }
-      }
-    } else if (vslot >= p.s_max) {
-      ok = false;
-      flags = PRCR_DERR_CAPACITY;
-    }
-  }
-  int64_t slot_id = -1, blk = 0, off = 0;
-  if (ok) {
-    if constexpr (kPaged) {
-      const int64_t lb = slot >= 0 ? slot / p.block_size : -1;
-      if (lb < 0 || lb >= p.max_blocks) {
+      } else if (vslot >= p.s_max) {
         ok = false;
         flags = PRCR_DERR_CAPACITY;
-      } else {
-        blk = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
-        if (blk < 0 || blk >= p.n_blocks) {
+      }
+    }
+    if (ok) {
+      if constexpr (kPaged) {
+        if (slot_flag != 0) {
+          ok = false;
+          flags = slot_flag;
+        } else if (blk < 0 || blk >= p.n_blocks) {
           ok = false;
           flags = PRCR_DERR_BLOCK;
         } else {
-          off = slot - lb * p.block_size;
           slot_id = blk * p.block_size + off;
         }
-      }
-    } else if (slot < 0 || slot >= p.s_max) {
-      ok = false;
-      flags = PRCR_DERR_CAPACITY;
-    } else {
-      slot_id = static_cast<int64_t>(b) * p.s_max + slot;
-    }
-  }
-  if (keys && grp == 0 && lane == 0) {
-    if (p.slot_mapping != nullptr) p.slot_mapping[g] = ok ? slot_id : -1;
-    if (flags != 0 && p.err != nullptr) atomicOr(p.err, flags);
-  }
-  if (!ok) return;
-
-  // Destination slot within a layer's block pool (paged only).
-  const size_t dst_pool = kPaged ? static_cast<size_t>(blk) * p.block_size + off : 0;
-  // Byte offset of (layer, head) row `row` of a cache slot: `pool` is the slot
-  // within a layer's block pool (paged), `sl` the sequence's slot (contiguous).
-  auto cache_offset = [&](int row, size_t pool, int64_t sl) -> size_t {
-    if constexpr (kPaged) {
-      const int l = row / p.n_kv_heads;
-      const int h = row - l * p.n_kv_heads;
-      return ((static_cast<size_t>(l) * p.n_blocks * p.block_size + pool) * p.n_kv_heads + h) *
-             kRowBytes;
-    } else {
-      return ((static_cast<size_t>(b) * rows_total + row) * p.s_max + sl) * kRowBytes;
-    }
-  };
-  auto dst_offset = [&](int row) -> size_t { return cache_offset(row, dst_pool, slot); };
-  auto src_offset = [&](int row) -> size_t {
-    return alias_v ? cache_offset(row, static_cast<size_t>(vpool), vslot)
-                   : static_cast<size_t>(row) * kRowBytes;
-  };
-  if (alias_v) {
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int row = row0 + u * RPI + r;
-      if (row < row_end) {
-        lo[u] = load16(src + src_offset(row));
-        hi[u] = load16(src + src_offset(row) + kHalfBytes);
+      } else if (slot < 0 || slot >= p.s_max) {
+        ok = false;
+        flags = PRCR_DERR_CAPACITY;
+      } else {
+        slot_id = static_cast<int64_t>(b) * p.s_max + slot;
       }
     }
-  }
-
-  // cos/sin of this token's angles (keys only): lane i computes pair i (mod P),
-  // then lane (r, c) gathers the pairs c*E .. c*E+E-1 of its two chunks.
-  double cs[E], sn[E];
-  if (keys) {
-    const int pair = lane % P;
-    const int ax = Map::axis(pair);
-    double sv, cv;
-    sincos((ax == 0 ? pt : (ax == 1 ? ph : pw)) * p.inv_freq[pair], &sv, &cv);
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      cs[e] = __shfl(cv, c * E + e);
-      sn[e] = __shfl(sv, c * E + e);
+    if (keys && grp == 0 && lane == 0) {
+      if (p.slot_mapping != nullptr) p.slot_mapping[g] = ok ? slot_id : -1;
+      if (flags != 0 && p.err != nullptr) atomicOr(p.err, flags);
     }
-  }
+    if (!ok) return;
 
-  for (int rb = row0; rb < row_end; rb += kStep) {
-    // next batch in flight while this one is stored
-    u32x4 nlo[kUnroll], nhi[kUnroll];
-    const int nb = rb + kStep;
+    // Destination slot within a layer's block pool (paged only).
+    const size_t dst_pool = kPaged ? static_cast<size_t>(blk) * p.block_size + off : 0;
+    // Byte offset of (layer, head) row `row` of a cache slot: `pool` is the slot
+    // within a layer's block pool (paged), `sl` the sequence's slot (contiguous).
+    auto cache_offset = [&](int row, size_t pool, int64_t sl) -> size_t {
+      if constexpr (kPaged) {
+        const int l = row / p.n_kv_heads;
+        const int h = row - l * p.n_kv_heads;
+        return ((static_cast<size_t>(l) * p.n_blocks * p.block_size + pool) * p.n_kv_heads + h) *
+               kRowBytes;
+      } else {
+        return ((static_cast<size_t>(b) * rows_total + row) * p.s_max + sl) * kRowBytes;
+      }
+    };
+    auto dst_offset = [&](int row) -> size_t { return cache_offset(row, dst_pool, slot); };
+    auto src_offset = [&](int row) -> size_t {
+      return alias_v ? cache_offset(row, static_cast<size_t>(vpool), vslot)
+                     : static_cast<size_t>(row) * kRowBytes;
+    };
+    if (alias_v) {
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int row = nb + u * RPI + r;
-      if (row < row_end) {
+      for (int u = 0; u < kUnroll; ++u) {
+        const int row = row0 + u * RPI + r;
+        if (row < row_end) {
+          lo[u] = load16(src + src_offset(row));
+          hi[u] = load16(src + src_offset(row) + kHalfBytes);
+        }
+      }
+    }
+
+    // cos/sin of this token's angles (keys only): lane i computes pair i (mod P),
+    // then lane (r, c) gathers the pairs c*E .. c*E+E-1 of its two chunks.
+    double cs[E], sn[E];
+    if (keys) {
+      const int pair = lane % P;
+      const int ax = Map::axis(pair);
+      double sv, cv;
+      sincos((ax == 0 ? pt : (ax == 1 ? ph : pw)) * p.inv_freq[pair], &sv, &cv);
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        cs[e] = __shfl(cv, c * E + e);
+        sn[e] = __shfl(sv, c * E + e);
+      }
+    }
+
+    // Rows rb .. rb + kStep - 1 of the batch held in lo/hi: rotated (keys) and
+    // stored.
+    auto store_batch = [&](int rb) {
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int row = rb + u * RPI + r;
+        if (row < row_end) {
+          u32x4 ol = lo[u], oh = hi[u];
+          if (keys) Store<T>::rotate(lo[u], hi[u], cs, sn, ol, oh);
+          const size_t d = dst_offset(row);
+          store16(dst + d, ol);
+          store16(dst + d + kHalfBytes, oh);
+        }
+      }
+    };
+    // The next batch is in flight while this one is stored.  Its loads are
+    // issued unconditionally (rows past the run reload its last row), so that
+    // the wait before the stores covers exactly this batch; the last batch,
+    // which has no next one, is stored after the loop.
+    int rb = row0;
+    for (; rb + kStep < row_end; rb += kStep) {
+      u32x4 nlo[kUnroll], nhi[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int row = min(rb + kStep + u * RPI + r, row_end - 1);
         nlo[u] = load16(src + src_offset(row));
         nhi[u] = load16(src + src_offset(row) + kHalfBytes);
       }
-    }
+      store_batch(rb);
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int row = rb + u * RPI + r;
-      if (row < row_end) {
-        u32x4 ol = lo[u], oh = hi[u];
-        if (keys) Store<T>::rotate(lo[u], hi[u], cs, sn, ol, oh);
-        const size_t d = dst_offset(row);
-        store16(dst + d, ol);
-        store16(dst + d + kHalfBytes, oh);
+      for (int u = 0; u < kUnroll; ++u) {
+        lo[u] = nlo[u];
+        hi[u] = nhi[u];
       }
     }
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      lo[u] = nlo[u];
-      hi[u] = nhi[u];
-    }
-  }
+    store_batch(rb);
+  };
+  if (keys)
+    half(std::true_type{});
+  else
+    half(std::false_type{});
 }
 
 constexpr int kWavesPerBlock = PRCR_WAVES_PER_BLOCK;
