@@ -153,6 +153,26 @@ def test_malformed_offsets_flagged():
     assert (slots.cpu().numpy() >= -1).all()
 
 
+@pytest.mark.parametrize("bad", [[0, 5, 5, 100], [-4, 5, 5, 8]])
+def test_malformed_offsets_fused(bad):
+    """The single-launch revisit with offsets outside [0, total_k]: the tokens of
+    the malformed sequence are skipped with PRCR_DERR_OFFSETS, and its range
+    reduction reads no index beyond the selection."""
+    w = workloads.custom(B=3, ks=(5, 0, 3), lens=(3, 4, 5))
+    case = Case(w)
+    mem, cache = case.memory(), case.cache()
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    _say(f"fused revisit with sel_off {bad}")
+    _, _, _, slots = prcr.revisit(case.rope(), mem, to_dev(np.array(bad, np.int32)), to_dev(w.sel_idx),
+                                  to_dev(w.p_txt), cache, to_dev(w.cache_len), "pcr", 2, err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) & prcr.DERR_OFFSETS
+    sl = slots.cpu().numpy()
+    skipped = slice(5, 8) if bad[-1] != 8 else slice(0, 5)
+    assert (sl[skipped] == -1).all()
+    assert (sl >= -1).all()
+
+
 def test_position_range_flag():
     """A PCR rational too large for exact double division is flagged and stays close."""
     w = workloads.custom(B=1, ks=(40,), lens=(7,), gh=12, gw=10)
