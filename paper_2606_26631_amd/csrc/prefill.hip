@@ -8,7 +8,9 @@
 // One wavefront covers PRCR_PF_ITERS x (rows per iteration) consecutive
 // (sequence, token, head) rows of the layer (8 at bf16, d 128: one token's 8
 // heads); a lane owns one 16-byte chunk of each half of a row, as in the rebind
-// kernel, and evaluates the cos/sin of its own pairs.
+// kernel.  A wave moves one batch of rows, so its latency is mostly the chain of
+// dependent loads before its stores: the kernel keeps that chain at two rounds
+// (three for a paged destination).
 #include <climits>
 #include <cmath>
 
@@ -24,7 +26,11 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kIters = PRCR_PF_ITERS;
 
-template <typename T, int D, class Map, bool kPaged>
+// kOneTok: n_kv_heads is a multiple of the rows per iteration, so the RPI-aligned
+// rows of an iteration are heads of one token.  Validity and slot are then
+// uniform across the wave, and one sincos per lane shared by shuffles covers the
+// token.  Otherwise each lane evaluates the E pairs of its own row.
+template <typename T, int D, class Map, bool kPaged, bool kOneTok>
 __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const PrefillParams p) {
   constexpr int P = D / 2;
   constexpr int E = Store<T>::kPerChunk;
@@ -42,47 +48,69 @@ __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const P
   if (base >= rows_all) return;
   const int r = lane / LPR;
   const int c = lane % LPR;
-  // With n_kv_heads a multiple of the rows per iteration, the RPI-aligned rows of
-  // an iteration are heads of one token: validity and slot are then uniform across
-  // the wave, and one sincos per lane shared by shuffles covers the token.
-  const bool one_token = (H % RPI) == 0;
 
-  // Row metadata and loads for all iterations first.
-  u32x4 kl[kIters], kh[kIters], vl[kIters], vh[kIters];
+  // The wave's loads are issued in two rounds, from indices that are always in
+  // range: first each row's sequence length, then together the raw rows of the
+  // live rows (those below n_tokens) and, per row, its token's position ids,
+  // visual index and sequence values, plus this lane's rotary frequency.  Vector
+  // loads complete in issue order, so a load issued only after another's value
+  // is used waits a round trip more.  Only a paged destination's block-table
+  // entry waits on these.
   int rb[kIters], rs[kIters], rh[kIters];
-  bool live[kIters];
+  int32_t nt[kIters];
+  int64_t Rc[kIters];
+  bool inr[kIters];
 #pragma unroll
   for (int u = 0; u < kIters; ++u) {
     const int64_t R = base + u * RPI + r;
-    live[u] = R < rows_all;
-    const int64_t Rc = live[u] ? R : 0;
-    rb[u] = static_cast<int>(Rc / (static_cast<int64_t>(p.s_src) * H));
-    const int64_t rem = Rc - static_cast<int64_t>(rb[u]) * p.s_src * H;
+    inr[u] = R < rows_all;
+    Rc[u] = inr[u] ? R : rows_all - 1;
+    rb[u] = static_cast<int>(Rc[u] / (static_cast<int64_t>(p.s_src) * H));
+    const int64_t rem = Rc[u] - static_cast<int64_t>(rb[u]) * p.s_src * H;
     rs[u] = static_cast<int>(rem / H);
     rh[u] = static_cast<int>(rem - static_cast<int64_t>(rs[u]) * H);
-    const int nt = p.n_tokens[rb[u]];
-    if (live[u] && (nt < 0 || nt > p.s_src) && rs[u] == 0 && rh[u] == 0 && c == 0 && p.err)
-      atomicOr(p.err, PRCR_DERR_INDEX);
-    live[u] = live[u] && rs[u] < min(max(nt, 0), p.s_src);
+    nt[u] = p.n_tokens[rb[u]];
+  }
+  const double inv_lane = p.inv_freq[lane % P];
+  u32x4 kl[kIters], kh[kIters], vl[kIters], vh[kIters];
+  int32_t cst[kIters], vis[kIters], nvis[kIters], pid[kIters][3];
+  bool live[kIters];
+#pragma unroll
+  for (int u = 0; u < kIters; ++u) {
+    const int64_t tok = static_cast<int64_t>(rb[u]) * p.s_src + rs[u];
+    cst[u] = p.cache_start[rb[u]];
+    nvis[u] = p.n_visual[rb[u]];
+    vis[u] = p.vis_index[tok];
+    pid[u][0] = p.pos[3 * tok + 0];
+    pid[u][1] = p.pos[3 * tok + 1];
+    pid[u][2] = p.pos[3 * tok + 2];
+    live[u] = inr[u] && rs[u] < min(max(nt[u], 0), p.s_src);
     if (live[u]) {
-      const size_t o = static_cast<size_t>(Rc) * kRowBytes + c * 16;
+      const size_t o = static_cast<size_t>(Rc[u]) * kRowBytes + c * 16;
       kl[u] = load_nt(static_cast<const char *>(p.raw_k) + o);
       kh[u] = load_nt(static_cast<const char *>(p.raw_k) + o + kHalfBytes);
       vl[u] = load_nt(static_cast<const char *>(p.raw_v) + o);
       vh[u] = load_nt(static_cast<const char *>(p.raw_v) + o + kHalfBytes);
     }
   }
+  // Per-row rotation: the lane's E frequencies, taken from the lanes that hold
+  // them while every lane is still active.
+  double inv[kOneTok ? 1 : E];
+  if constexpr (!kOneTok) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) inv[e] = __shfl(inv_lane, c * E + e);
+  }
 
 #pragma unroll
   for (int u = 0; u < kIters; ++u) {
-    if (!live[u]) continue;
     const int b = rb[u], s = rs[u], h = rh[u];
-    const int64_t tok = static_cast<int64_t>(b) * p.s_src + s;
-    const int32_t *pp = p.pos + 3 * tok;
-    const double pt = pp[0], ph = pp[1], pw = pp[2];
+    if (inr[u] && (nt[u] < 0 || nt[u] > p.s_src) && s == 0 && h == 0 && c == 0 && p.err)
+      atomicOr(p.err, PRCR_DERR_INDEX);
+    if (!live[u]) continue;
+    const double pt = pid[u][0], ph = pid[u][1], pw = pid[u][2];
 
     // Standard cache: rotated key and value at slot cache_start[b] + s (Eq. (4)).
-    const int64_t slot = static_cast<int64_t>(p.cache_start[b]) + s;
+    const int64_t slot = static_cast<int64_t>(cst[u]) + s;
     int64_t d = -1;
     int flag = 0;
     if constexpr (kPaged) {
@@ -106,13 +134,13 @@ __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const P
     }
     if (d >= 0) {
       double cs[E], sn[E];
-      if (one_token) {
+      if constexpr (kOneTok) {
         // All rows of this iteration belong to one token: lane i evaluates pair i
         // (mod P) and each lane gathers its E pairs with shuffles.
         const int pair = lane % P;
         const int ax = Map::axis(pair);
         double sv, cv;
-        sincos((ax == 0 ? pt : (ax == 1 ? ph : pw)) * p.inv_freq[pair], &sv, &cv);
+        sincos((ax == 0 ? pt : (ax == 1 ? ph : pw)) * inv_lane, &sv, &cv);
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           cs[e] = __shfl(cv, c * E + e);
@@ -121,9 +149,8 @@ __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const P
       } else {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-          const int pair = c * E + e;
-          const int ax = Map::axis(pair);
-          sincos((ax == 0 ? pt : (ax == 1 ? ph : pw)) * p.inv_freq[pair], &sn[e], &cs[e]);
+          const int ax = Map::axis(c * E + e);
+          sincos((ax == 0 ? pt : (ax == 1 ? ph : pw)) * inv[e], &sn[e], &cs[e]);
         }
       }
       u32x4 ol, oh;
@@ -137,9 +164,9 @@ __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const P
     }
 
     // Raw Visual Evidence Memory: raw rows of visual tokens (Eq. (6)-(7)).
-    const int m = p.vis_index[tok];
+    const int m = vis[u];
     if (m >= 0) {
-      if (m >= p.max_visual || m >= p.n_visual[b]) {
+      if (m >= p.max_visual || m >= nvis[u]) {
         flag |= PRCR_DERR_INDEX;
       } else {
         const size_t mo = (((static_cast<size_t>(b) * p.max_visual + m) * p.n_layers + p.layer) * H + h) *
@@ -158,9 +185,9 @@ __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const P
         }
         if (p.write_coords && h == 0 && c == 0) {
           int32_t *co = p.coords + (static_cast<int64_t>(b) * p.max_visual + m) * 3;
-          co[0] = pp[0];
-          co[1] = pp[1];
-          co[2] = pp[2];
+          co[0] = pid[u][0];
+          co[1] = pid[u][1];
+          co[2] = pid[u][2];
         }
       }
     }
@@ -177,8 +204,12 @@ hipError_t launch_one(const PrefillParams &p, hipStream_t stream) {
   int64_t blocks = (rows_all + per_block - 1) / per_block;
   if (blocks < 1) blocks = 1;
   if (!grid_fits(blocks, kWaves * kWave)) return hipErrorInvalidConfiguration;
-  prefill_capture_kernel<T, D, Map, kPaged><<<dim3(static_cast<unsigned>(blocks)), kWaves * kWave, 0,
-                                              stream>>>(p);
+  if (p.n_kv_heads % RPI == 0)
+    prefill_capture_kernel<T, D, Map, kPaged, true>
+        <<<dim3(static_cast<unsigned>(blocks)), kWaves * kWave, 0, stream>>>(p);
+  else
+    prefill_capture_kernel<T, D, Map, kPaged, false>
+        <<<dim3(static_cast<unsigned>(blocks)), kWaves * kWave, 0, stream>>>(p);
   return hipGetLastError();
 }
 
