@@ -15,7 +15,8 @@ slots per sequence (power_of_two_capacity: 2 MiB cache rows, which the memory
 channels absorb faster), with a key-only memory, with 1-D rotary positions (the
 rotary form of InternVL3.5, the paper's other model family), at one GPU's share of 8-way
 KV-head parallelism, over four video revisits and at small selections, and time
-the prefill capture, raw-memory store and decode attention kernels.
+the prefill capture (at 36 x 8 and 28 x 4 KV heads), raw-memory store and decode
+attention kernels.
 
 Prints one JSON line.  `value` = rebound (sequence, token, layer, KV-head)
 entries per second over the timed steps.  `roofline` is for the dominant kernel
@@ -250,18 +251,19 @@ def small_k_latency(dev, reps=200):
     return out
 
 
-def prefill_capture_bw(dev, steps=20):
+def prefill_capture_bw(dev, steps=20, NL=36, H=8):
     """Bandwidth of the fused prefill capture (one layer per call) at the 32-sequence
-    shape: 32 prompts of 256 text + 64x32 visual + 256 text tokens, 36 layers x 8 KV
-    heads, d 128, bf16, interleaved M-RoPE.  Algorithmic bytes per call: read raw K+V
-    of every prompt row, write K+V into the cache, and K+V into the memory for the
-    visual rows (2 * d * 2 bytes each)."""
+    shape: 32 prompts of 256 text + 64x32 visual + 256 text tokens, NL layers x H KV
+    heads (36 x 8 by default; 28 x 4 is the paged workload's model shape), d 128,
+    bf16, interleaved M-RoPE.  Algorithmic bytes per call: read raw K+V of every
+    prompt row, write K+V into the cache, and K+V into the memory for the visual
+    rows (2 * d * 2 bytes each)."""
     import numpy as np
     import torch
 
     import paper_2606_26631_amd as prcr
     import workloads
-    B, NL, H, D = 32, 36, 8, 128
+    B, D = 32, 128
     pos, vis, n_tok, n_vis = workloads.prompt(B, n_before=(256,) * B, grid=((64, 32),) * B,
                                               n_after=(256,) * B, frames=(1,) * B)
     S = pos.shape[1]
@@ -308,7 +310,7 @@ def prefill_capture_bw(dev, steps=20):
             "mean_launch_us": round(mean_s * 1e6, 2), "algorithmic_bytes_per_call": nbytes,
             "achieved": round(nbytes / mean_s / 1e9, 1), "unit": "GB/s",
             "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4),
-            "traffic": load_traffic("prefill_capture", "prefill")}
+            "traffic": load_traffic("prefill_capture" if H == 8 else f"prefill_capture_{H}kv", "prefill")}
 
 
 def store_raw_bw(dev, steps=20):
@@ -737,6 +739,7 @@ def main():
         sections.append(("small_workloads", lambda: small_workloads(dev)))
     if not args.no_prefill:
         sections.append(("prefill_capture", lambda: prefill_capture_bw(dev)))
+        sections.append(("prefill_capture_4kv_heads", lambda: prefill_capture_bw(dev, NL=28, H=4)))
         sections.append(("store_raw", lambda: store_raw_bw(dev)))
     if not args.no_decode:
         sections.append(("decode_attention", lambda: decode_attention_bw(dev)))
