@@ -50,24 +50,33 @@ __global__ __launch_bounds__(kThreads) void reassign_kernel(const ReassignParams
   }
   const int K = s1 - s0;
   const int64_t L = p.l_ext;
+  // The first selected index of this thread is loaded together with the token
+  // count (it does not depend on it).
+  const int m_first = tid < K ? p.sel_idx[s0 + tid] : -1;
   const int nvis = min(p.n_visual[b], p.max_visual);
   const int32_t *coords_b = p.coords + static_cast<int64_t>(b) * p.max_visual * 3;
 
-  // Eq. (8): per-axis range over the valid selected tokens.
+  // Eq. (8): per-axis range over the valid selected tokens.  A thread keeps the
+  // index and coordinates of its first token for the second pass (every token,
+  // when K <= kThreads), so that pass needs no loads for it.
   int lo[3] = {INT_MAX, INT_MAX, INT_MAX};
   int hi[3] = {INT_MIN, INT_MIN, INT_MIN};
   int bad = 0;
+  int c_first[3] = {0, 0, 0};
   for (int j = tid; j < K; j += kThreads) {
-    const int m = p.sel_idx[s0 + j];
+    const int m = j == tid ? m_first : p.sel_idx[s0 + j];
     if (m < 0 || m >= nvis) {
       bad = 1;
       continue;
     }
+    int cc[3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a) cc[a] = coords_b[3 * m + a];
 #pragma unroll
     for (int a = 0; a < 3; ++a) {
-      const int c = coords_b[3 * m + a];
-      lo[a] = min(lo[a], c);
-      hi[a] = max(hi[a], c);
+      if (j == tid) c_first[a] = cc[a];
+      lo[a] = min(lo[a], cc[a]);
+      hi[a] = max(hi[a], cc[a]);
     }
   }
 #pragma unroll
@@ -100,16 +109,23 @@ __global__ __launch_bounds__(kThreads) void reassign_kernel(const ReassignParams
 
   int range_bad = 0;
   for (int j = tid; j < K; j += kThreads) {
-    const int m = p.sel_idx[s0 + j];
+    const int m = j == tid ? m_first : p.sel_idx[s0 + j];
     double *out = p.new_pos + 3 * static_cast<int64_t>(s0 + j);
     if (m < 0 || m >= nvis) {
       out[0] = out[1] = out[2] = __builtin_nan("");
       continue;
     }
-    bool rb = false;
+    // All three coordinates are in registers before the first store (the stores
+    // could otherwise alias them and force a reload after each one).
+    int cc[3];
 #pragma unroll
-    for (int a = 0; a < 3; ++a)
-      out[a] = reassigned(p.mode, p_txt, L, K, j, lo[a], hi[a], coords_b[3 * m + a], &rb);
+    for (int a = 0; a < 3; ++a) cc[a] = j == tid ? c_first[a] : coords_b[3 * m + a];
+    bool rb = false;
+    double v[3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a) v[a] = reassigned(p.mode, p_txt, L, K, j, lo[a], hi[a], cc[a], &rb);
+#pragma unroll
+    for (int a = 0; a < 3; ++a) out[a] = v[a];
     range_bad |= rb ? 1 : 0;
   }
 
