@@ -309,20 +309,61 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
   }
 }
 
+// Merge of one query head's split partials.  Each split's (max, sum) is read by
+// one thread, D splits at a time, so that the reads go out together instead of
+// one after another's use; the weights pass through LDS, and every thread then
+// accumulates its feature over the splits in split order with the same fused
+// multiply-adds as a sequential merge (an empty split adds exact zeros).
 template <int D>
 __global__ __launch_bounds__(D) void decode_combine_kernel(const DecodeParams p) {
+  __shared__ float s_red[D / kWave];
+  __shared__ float s_w[D], s_l[D];
   const int qh = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
-  const float *ws = p.ws + (static_cast<int64_t>(b) * p.n_q_heads + qh) * p.n_split * (D + 2);
-  float M = -FLT_MAX;
-  for (int s = 0; s < p.n_split; ++s)
-    if (ws[s * (D + 2) + D + 1] > 0.f) M = fmaxf(M, ws[s * (D + 2) + D]);
+  const int lane = d & (kWave - 1), wave = d / kWave;
+  const int ns = p.n_split;
+  const float *ws = p.ws + (static_cast<int64_t>(b) * p.n_q_heads + qh) * ns * (D + 2);
+  // Largest max over the splits that saw a key.  Both values of a split are
+  // read before either is used; a thread keeps those of its first split (every
+  // split, when n_split <= D) for the second pass.
+  float M = -FLT_MAX, l_first = 0.f, m_first = -FLT_MAX;
+  for (int s0 = 0; s0 < ns; s0 += D) {
+    const int s = min(s0 + d, ns - 1);
+    const float l = ws[static_cast<int64_t>(s) * (D + 2) + D + 1];
+    const float m = ws[static_cast<int64_t>(s) * (D + 2) + D];
+    const bool used = s0 + d < ns && l > 0.f;
+    M = used ? fmaxf(M, m) : M;
+    if (s0 == 0) {
+      l_first = used ? l : 0.f;
+      m_first = m;
+    }
+  }
+  for (int o = kWave / 2; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  if (lane == 0) s_red[wave] = M;
+  __syncthreads();
+  M = s_red[0];
+#pragma unroll
+  for (int w = 1; w < D / kWave; ++w) M = fmaxf(M, s_red[w]);
   float Ls = 0.f, Os = 0.f;
-  for (int s = 0; s < p.n_split; ++s) {
-    const float l = ws[s * (D + 2) + D + 1];
-    if (l > 0.f) {
-      const float w = exp2_fast(ws[s * (D + 2) + D] - M);
-      Ls += l * w;
-      Os += ws[s * (D + 2) + d] * w;
+  for (int s0 = 0; s0 < ns; s0 += D) {
+    const int s = s0 + d;
+    float l = l_first, m = m_first;
+    if (s0 > 0) {
+      const int sc = min(s, ns - 1);
+      l = ws[static_cast<int64_t>(sc) * (D + 2) + D + 1];
+      m = ws[static_cast<int64_t>(sc) * (D + 2) + D];
+      l = s < ns && l > 0.f ? l : 0.f;
+    }
+    const float w = l > 0.f ? exp2_fast(m - M) : 0.f;
+    __syncthreads();
+    s_w[d] = w;
+    s_l[d] = l;
+    __syncthreads();
+    const int cnt = min(D, ns - s0);
+    const float *o = ws + static_cast<int64_t>(s0) * (D + 2) + d;
+#pragma unroll 4
+    for (int k = 0; k < cnt; ++k) {
+      Ls = fmaf(s_l[k], s_w[k], Ls);
+      Os = fmaf(o[static_cast<int64_t>(k) * (D + 2)], s_w[k], Os);
     }
   }
   p.out[(static_cast<int64_t>(b) * p.n_q_heads + qh) * D + d] = Ls > 0.f ? Os / Ls : 0.f;
