@@ -41,7 +41,7 @@ def test_library_exports_every_declared_function():
     assert {"prcr_store_raw", "prcr_reassign_coords", "prcr_rebind_inject"} <= set(names)
     for n in names:
         assert hasattr(L, n), f"{n} declared in prcr.h but not exported"
-    assert L.prcr_version() == 10301
+    assert L.prcr_version() == 10302
 
 
 def test_status_strings():
