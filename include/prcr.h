@@ -190,7 +190,13 @@ prcr_status prcr_store_raw(const prcr_mem *mem, int32_t layer,
  * outside [0, n_visual[b]) gets NaN positions and PRCR_DERR_INDEX and is left out
  * of the range.  PCR/UIR positions are exact (correctly rounded) while the
  * rational's numerator and denominator stay below 2^52; beyond that the value
- * is within a few ulp and PRCR_DERR_RANGE is raised.
+ * is within a few ulp and PRCR_DERR_RANGE is raised.  A next text position
+ * outside the int32 range is saturated to INT32_MAX (or INT32_MIN), never
+ * wrapped, and PRCR_DERR_RANGE is raised.
+ *
+ * next_pos may be p_txt itself (an in-place advance: each sequence reads its own
+ * p_txt before writing its next_pos); it must not share memory with sel_off or
+ * n_visual (PRCR_ERR_ALIAS).
  */
 prcr_status prcr_reassign_coords(const prcr_mem *mem,
                                  const int32_t *sel_off, const int32_t *sel_idx,
@@ -208,7 +214,7 @@ prcr_status prcr_reassign_coords(const prcr_mem *mem,
  *   new_pos       double [total_k][3] (e.g. from prcr_reassign_coords)
  *   cache_len     int32 [batch] in: first free slot of each sequence
  *   new_cache_len int32 [batch] out (may be NULL): cache_len[b] + K_b; must
- *                 not alias cache_len
+ *                 not share memory with cache_len or sel_off (PRCR_ERR_ALIAS)
  *   slot_mapping  int64 [total_k] out (may be NULL)
  *
  * Token j of sequence b goes to slot cache_len[b] + j.  Key elements are
@@ -272,6 +278,14 @@ prcr_status prcr_prefill_capture(const prcr_rope *rope, const prcr_mem *mem, int
  * its own sequence's coordinate ranges, reading K_b coordinates, so for large
  * selections (hundreds of tokens per sequence and more) the two-call path is
  * faster.
+ *
+ * Aliasing.  In the single launch, one wave per sequence writes next_pos[b] (and
+ * the first workgroup the new lengths) while every other wave still reads p_txt,
+ * cache_len, sel_off and n_visual.  So next_pos must not share memory with
+ * p_txt, cache_len, sel_off, n_visual or new_cache_len, and new_cache_len not
+ * with p_txt, cache_len or sel_off: such calls return PRCR_ERR_ALIAS before any
+ * launch.  (Advancing p_txt in place, as a decode loop may, needs a separate
+ * next_pos buffer here, or the two-call path.)
  */
 prcr_status prcr_revisit(const prcr_rope *rope, const prcr_mem *mem,
                          const int32_t *sel_off, const int32_t *sel_idx, int32_t total_k,

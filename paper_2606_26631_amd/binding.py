@@ -245,6 +245,20 @@ def _selection(mem: Memory, sel_off, sel_idx):
     return int(sel_idx.shape[0])
 
 
+def _overlap(a, b) -> bool:
+    """Whether two tensors share any byte of device memory."""
+    if a is None or b is None or a.numel() == 0 or b.numel() == 0:
+        return False
+    x, y = a.data_ptr(), b.data_ptr()
+    return x < y + b.numel() * b.element_size() and y < x + a.numel() * a.element_size()
+
+
+def _no_alias(pairs):
+    for (oname, o), (iname, i) in pairs:
+        if _overlap(o, i):
+            raise ValueError(f"{oname} must not share memory with {iname}")
+
+
 def _shape(t, name, shape):
     if tuple(t.shape) != tuple(shape):
         raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
@@ -297,6 +311,8 @@ def reassign_coords(mem: Memory, sel_off, sel_idx, p_txt, mode: str = "pcr", l_e
     _need(next_pos, "next_pos", torch.int32, 1, mem.device)
     _shape(new_pos, "new_pos", (total_k, 3))
     _shape(next_pos, "next_pos", (B,))
+    _no_alias([(("next_pos", next_pos), ("sel_off", sel_off)),
+               (("next_pos", next_pos), ("mem.n_visual", mem.n_visual))])
     _err(err, mem.device)
     if mode not in MODES:
         raise ValueError(f"mode must be one of {sorted(MODES)}")
@@ -327,8 +343,8 @@ def rebind_inject(rope: Rope, mem: Memory, sel_off, sel_idx, new_pos, cache: Cac
     _need(slot_mapping, "slot_mapping", torch.int64, 1, mem.device)
     _shape(new_cache_len, "new_cache_len", (B,))
     _shape(slot_mapping, "slot_mapping", (total_k,))
-    if new_cache_len.data_ptr() == cache_len.data_ptr():
-        raise ValueError("new_cache_len must not alias cache_len")
+    _no_alias([(("new_cache_len", new_cache_len), ("cache_len", cache_len)),
+               (("new_cache_len", new_cache_len), ("sel_off", sel_off))])
     _err(err, mem.device)
     st = lib().prcr_rebind_inject(ctypes.byref(rope.to_c()), ctypes.byref(mem.to_c()), _ptr(sel_off),
                                   _ptr(sel_idx), total_k, _ptr(new_pos), ctypes.byref(cache.to_c()),
@@ -369,8 +385,16 @@ def revisit(rope: Rope, mem: Memory, sel_off, sel_idx, p_txt, cache: Cache, cach
     _shape(next_pos, "next_pos", (B,))
     _shape(new_cache_len, "new_cache_len", (B,))
     _shape(slot_mapping, "slot_mapping", (total_k,))
-    if new_cache_len.data_ptr() == cache_len.data_ptr():
-        raise ValueError("new_cache_len must not alias cache_len")
+    # Every wave of the single launch reads p_txt, cache_len, the offsets and the
+    # visual counts while some waves write next_pos and the new lengths.
+    _no_alias([(("next_pos", next_pos), ("p_txt", p_txt)),
+               (("next_pos", next_pos), ("cache_len", cache_len)),
+               (("next_pos", next_pos), ("sel_off", sel_off)),
+               (("next_pos", next_pos), ("mem.n_visual", mem.n_visual)),
+               (("next_pos", next_pos), ("new_cache_len", new_cache_len)),
+               (("new_cache_len", new_cache_len), ("cache_len", cache_len)),
+               (("new_cache_len", new_cache_len), ("sel_off", sel_off)),
+               (("new_cache_len", new_cache_len), ("p_txt", p_txt))])
     _err(err, mem.device)
     if mode not in MODES:
         raise ValueError(f"mode must be one of {sorted(MODES)}")
@@ -468,3 +492,4 @@ def decode_attention(rope: Rope, cache: Cache, layer: int, q, q_pos, cache_len, 
                                      _ptr(err), _stream(stream, cache.device))
     _check("prcr_decode_attention", st)
     return out
+

@@ -11,19 +11,20 @@ using namespace prcr;
 
 namespace {
 
-constexpr int32_t kVersion = 1 * 10000 + 3 * 100 + 2;
+constexpr int32_t kVersion = 1 * 10000 + 3 * 100 + 3;
 constexpr int64_t kMaxDecodeSlots = int64_t{1} << 30;   // decode: cache capacity per sequence
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// Whether the byte ranges [a, a + na) and [b, b + nb) share a byte (null never does).
+bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
+  if (a == nullptr || b == nullptr || na == 0 || nb == 0) return false;
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
 int elem_bytes(prcr_dtype d) { return d == PRCR_F32 ? 4 : 2; }
 
-// A launcher's own refusal of a grid too large for one dispatch is a size error
-// found before any HIP call; anything else the runtime reports is a launch error.
-prcr_status launch_status(hipError_t e) {
-  if (e == hipSuccess) return PRCR_OK;
-  return e == hipErrorInvalidConfiguration ? PRCR_ERR_SHAPE : PRCR_ERR_HIP;
-}
 
 prcr_status check_rope(const prcr_rope *rope) {
   if (rope == nullptr) return PRCR_ERR_NULL;
@@ -86,6 +87,11 @@ prcr_status check_cache(const prcr_cache *cache) {
 }
 
 }  // namespace
+
+prcr_status prcr::launch_status(hipError_t e) {
+  if (e == hipSuccess) return PRCR_OK;
+  return e == hipErrorInvalidConfiguration ? PRCR_ERR_SHAPE : PRCR_ERR_HIP;
+}
 
 extern "C" {
 
@@ -168,6 +174,12 @@ prcr_status prcr_reassign_coords(const prcr_mem *mem, const int32_t *sel_off, co
   if (!aligned(p_txt, 4) || !aligned(next_pos, 4) || (new_pos != nullptr && !aligned(new_pos, 8)) ||
       (err_flag != nullptr && !aligned(err_flag, 4)))
     return PRCR_ERR_ALIGN;
+  // Sequence b's workgroup writes next_pos[b] while the others read their own
+  // offsets and visual counts.  (next_pos may alias p_txt: a workgroup reads only
+  // its own p_txt[b], before it writes next_pos[b].)
+  const size_t nb4 = static_cast<size_t>(mem->batch) * 4;
+  if (overlaps(next_pos, nb4, sel_off, nb4 + 4) || overlaps(next_pos, nb4, mem->n_visual, nb4))
+    return PRCR_ERR_ALIAS;
   ReassignParams p{};
   p.coords = mem->coords;
   p.n_visual = mem->n_visual;
@@ -209,7 +221,11 @@ prcr_status prepare_rebind(const prcr_rope *rope, const prcr_mem *mem, const int
       (slot_mapping != nullptr && !aligned(slot_mapping, 8)) ||
       (err_flag != nullptr && !aligned(err_flag, 4)))
     return PRCR_ERR_ALIGN;
-  if (new_cache_len != nullptr && new_cache_len == cache_len) return PRCR_ERR_ALIAS;
+  // The first workgroup writes the new lengths while the others still read the
+  // old lengths and the offsets.
+  const size_t nb4 = static_cast<size_t>(mem->batch) * 4;
+  if (overlaps(new_cache_len, nb4, cache_len, nb4) || overlaps(new_cache_len, nb4, sel_off, nb4 + 4))
+    return PRCR_ERR_ALIAS;
   *map = axis_map_id(*rope);
   if (*map == AxisMapId::kUnsupported) return PRCR_ERR_UNSUPPORTED;
 
@@ -351,12 +367,13 @@ prcr_status prcr_decode_workspace_size(const prcr_cache *cache, int32_t batch, i
   return PRCR_OK;
 }
 
-prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache, prcr_dtype dtype,
-                                  int32_t batch, int32_t n_layers, int32_t n_kv_heads, int32_t layer,
-                                  const void *q, int32_t n_q_heads, const int32_t *q_pos,
-                                  const int32_t *cache_len, float scale, float *out,
-                                  void *workspace, size_t workspace_bytes, int32_t *err_flag,
-                                  hipStream_t stream) {
+}  // extern "C"
+
+prcr_status prcr::prepare_decode(const prcr_rope *rope, const prcr_cache *cache, prcr_dtype dtype,
+                                 int32_t batch, int32_t n_layers, int32_t n_kv_heads, int32_t layer,
+                                 const void *q, int32_t n_q_heads, const int32_t *q_pos,
+                                 const int32_t *cache_len, float scale, float *out,
+                                 int32_t *err_flag, DecodeParams *out_params, size_t *ws_bytes) {
   prcr_status st = check_rope(rope);
   if (st != PRCR_OK) return st;
   if (dtype != PRCR_F32 && dtype != PRCR_BF16) return PRCR_ERR_DTYPE;
@@ -365,16 +382,14 @@ prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache
   if (st != PRCR_OK) return st;
   st = check_cache(cache);
   if (st != PRCR_OK) return st;
-  if (q == nullptr || q_pos == nullptr || cache_len == nullptr || out == nullptr ||
-      workspace == nullptr)
-    return PRCR_ERR_NULL;
+  if (q == nullptr || q_pos == nullptr || cache_len == nullptr || out == nullptr) return PRCR_ERR_NULL;
   if (n_layers < 1 || layer < 0 || layer >= n_layers || !std::isfinite(scale)) return PRCR_ERR_SHAPE;
-  const size_t need = static_cast<size_t>(batch) * n_q_heads * n_split * (rope->head_dim + 2) * sizeof(float);
-  if (workspace_bytes < need) return PRCR_ERR_SHAPE;
   if (!aligned(q, 16) || !aligned(q_pos, 4) || !aligned(cache_len, 4) || !aligned(out, 4) ||
-      !aligned(workspace, 4) || (err_flag != nullptr && !aligned(err_flag, 4)))
+      (err_flag != nullptr && !aligned(err_flag, 4)))
     return PRCR_ERR_ALIGN;
-  DecodeParams p{};
+  *ws_bytes = static_cast<size_t>(batch) * n_q_heads * n_split * (rope->head_dim + 2) * sizeof(float);
+  DecodeParams &p = *out_params;
+  p = DecodeParams{};
   p.q = q;
   p.q_pos = q_pos;
   p.cache_len = cache_len;
@@ -382,7 +397,7 @@ prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache
   p.cache_v = cache->v;
   p.block_table = cache->block_table;
   p.out = out;
-  p.ws = static_cast<float *>(workspace);
+  p.ws = nullptr;
   p.err = err_flag;
   p.batch = batch;
   p.n_layers = n_layers;
@@ -401,8 +416,27 @@ prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache
   p.scale = scale;
   for (int i = 0; i < rope->head_dim / 2; ++i)
     p.inv_freq[i] = std::pow(rope->theta, -(2.0 * i) / rope->head_dim);
-  const hipError_t e = launch_decode(p, dtype, rope->head_dim, cache->paged != 0, stream);
-  return launch_status(e);
+  return PRCR_OK;
+}
+
+extern "C" {
+
+prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache, prcr_dtype dtype,
+                                  int32_t batch, int32_t n_layers, int32_t n_kv_heads, int32_t layer,
+                                  const void *q, int32_t n_q_heads, const int32_t *q_pos,
+                                  const int32_t *cache_len, float scale, float *out,
+                                  void *workspace, size_t workspace_bytes, int32_t *err_flag,
+                                  hipStream_t stream) {
+  DecodeParams p;
+  size_t need = 0;
+  const prcr_status st = prepare_decode(rope, cache, dtype, batch, n_layers, n_kv_heads, layer, q,
+                                        n_q_heads, q_pos, cache_len, scale, out, err_flag, &p, &need);
+  if (st != PRCR_OK) return st;
+  if (workspace == nullptr) return PRCR_ERR_NULL;
+  if (workspace_bytes < need) return PRCR_ERR_SHAPE;
+  if (!aligned(workspace, 4)) return PRCR_ERR_ALIGN;
+  p.ws = static_cast<float *>(workspace);
+  return launch_status(launch_decode(p, dtype, rope->head_dim, cache->paged != 0, stream));
 }
 
 prcr_status prcr_revisit(const prcr_rope *rope, const prcr_mem *mem, const int32_t *sel_off,
@@ -420,6 +454,16 @@ prcr_status prcr_revisit(const prcr_rope *rope, const prcr_mem *mem, const int32
   if (mode < PRCR_MODE_PCR || mode > PRCR_MODE_PCR_RIGHT || l_ext < 0) return PRCR_ERR_MODE;
   if (!aligned(p_txt, 4) || !aligned(next_pos, 4) || (new_pos != nullptr && !aligned(new_pos, 8)))
     return PRCR_ERR_ALIGN;
+  // One wave per sequence writes next_pos[b] (and the first workgroup the new
+  // lengths) while every other wave of the launch still reads p_txt, cache_len,
+  // the offsets and the visual counts: none of them may share memory with an
+  // output, and the two outputs may not share memory with each other.  (An
+  // in-place advance of p_txt needs the two-call path or a separate buffer.)
+  const size_t nb4 = static_cast<size_t>(mem->batch) * 4;
+  if (overlaps(next_pos, nb4, p_txt, nb4) || overlaps(next_pos, nb4, cache_len, nb4) ||
+      overlaps(next_pos, nb4, sel_off, nb4 + 4) || overlaps(next_pos, nb4, mem->n_visual, nb4) ||
+      overlaps(next_pos, nb4, new_cache_len, nb4) || overlaps(new_cache_len, nb4, p_txt, nb4))
+    return PRCR_ERR_ALIAS;
   p.coords = mem->coords;
   p.p_txt = p_txt;
   p.pos_out = new_pos;

@@ -80,4 +80,19 @@ __device__ __forceinline__ int64_t next_text_position(int mode, int64_t p_txt, i
   return p_txt + 1;
 }
 
+// The next text position as the int32 the ABI returns: a value outside the
+// int32 range is saturated to its nearest end and *range_bad is set (the caller
+// then reports PRCR_DERR_RANGE), never wrapped.
+__device__ __forceinline__ int32_t next_pos_int32(int64_t next, bool *range_bad) {
+  if (next > INT32_MAX) {
+    *range_bad = true;
+    return INT32_MAX;
+  }
+  if (next < INT32_MIN) {
+    *range_bad = true;
+    return INT32_MIN;
+  }
+  return static_cast<int32_t>(next);
+}
+
 }  // namespace prcr

@@ -161,4 +161,17 @@ hipError_t launch_decode(const DecodeParams &p, prcr_dtype dtype, int head_dim, 
                          hipStream_t stream);
 int decode_splits(int64_t capacity, int batch, int n_kv_heads);
 
+// A launcher's own refusal of a grid too large for one dispatch is a size error
+// found before any HIP call (PRCR_ERR_SHAPE); anything else the runtime reports
+// is a launch error (PRCR_ERR_HIP).
+prcr_status launch_status(hipError_t e);
+
+// Host checks and parameter block shared by the decode entry points: everything
+// but the split-K workspace pointer, whose byte size is returned in *ws_bytes.
+prcr_status prepare_decode(const prcr_rope *rope, const prcr_cache *cache, prcr_dtype dtype,
+                           int32_t batch, int32_t n_layers, int32_t n_kv_heads, int32_t layer,
+                           const void *q, int32_t n_q_heads, const int32_t *q_pos,
+                           const int32_t *cache_len, float scale, float *out, int32_t *err_flag,
+                           DecodeParams *out_params, size_t *ws_bytes);
+
 }  // namespace prcr

@@ -42,8 +42,9 @@ __global__ __launch_bounds__(kThreads) void reassign_kernel(const ReassignParams
   if (b == p.batch - 1 && s1 != p.total_k) offsets_ok = false;
   if (!offsets_ok) {
     if (tid == 0) {
-      p.next_pos[b] = static_cast<int32_t>(p_txt + 1);
-      if (p.err != nullptr) atomicOr(p.err, PRCR_DERR_OFFSETS);
+      bool nb = false;
+      p.next_pos[b] = next_pos_int32(p_txt + 1, &nb);
+      if (p.err != nullptr) atomicOr(p.err, PRCR_DERR_OFFSETS | (nb ? PRCR_DERR_RANGE : 0));
     }
     // Out-of-range offsets leave this sequence's positions unwritten.
     if (!(s0 >= 0 && s0 <= s1 && s1 <= p.total_k)) return;
@@ -134,8 +135,10 @@ __global__ __launch_bounds__(kThreads) void reassign_kernel(const ReassignParams
     for (int a = 0; a < 3; ++a)
       span = max(span, static_cast<int64_t>(hi[a]) - static_cast<int64_t>(lo[a]));
     const int64_t next = next_text_position(p.mode, p_txt, K, any_valid, span);
-    p.next_pos[b] = static_cast<int32_t>(next);
-    if (bad && p.err != nullptr) atomicOr(p.err, PRCR_DERR_INDEX);
+    bool nb = false;
+    p.next_pos[b] = next_pos_int32(next, &nb);
+    if ((bad || nb) && p.err != nullptr)
+      atomicOr(p.err, (bad ? PRCR_DERR_INDEX : 0) | (nb ? PRCR_DERR_RANGE : 0));
   }
   if (range_bad && p.err != nullptr) atomicOr(p.err, PRCR_DERR_RANGE);
 }

@@ -113,8 +113,11 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
     for (int b = threadIdx.x; b < p.batch; b += blockDim.x) {
       const int kb = p.sel_off[b + 1] - p.sel_off[b];
       if (p.new_cache_len != nullptr) p.new_cache_len[b] = p.cache_len[b] + kb;
-      if (kFused && kb == 0)
-        p.next_pos[b] = static_cast<int32_t>(next_text_position(p.mode, p.p_txt[b], 0, false, 0));
+      if (kFused && kb == 0) {
+        bool nb = false;
+        p.next_pos[b] = next_pos_int32(next_text_position(p.mode, p.p_txt[b], 0, false, 0), &nb);
+        if (nb && p.err != nullptr) atomicOr(p.err, PRCR_DERR_RANGE);
+      }
     }
   }
   if (L >= n_work) return;
@@ -271,7 +274,10 @@ __global__ __launch_bounds__(kWaves * kWave) void rebind_inject_kernel(const Reb
                                                max(static_cast<int64_t>(hi1) - lo1,
                                                    static_cast<int64_t>(hi2) - lo2))
                                          : 0;
-          p.next_pos[b] = static_cast<int32_t>(next_text_position(p.mode, ptxt, K, any_valid, span));
+          bool next_bad = false;
+          p.next_pos[b] = next_pos_int32(next_text_position(p.mode, ptxt, K, any_valid, span),
+                                         &next_bad);
+          if (next_bad && p.err != nullptr) atomicOr(p.err, PRCR_DERR_RANGE);
         }
         if (ok && range_bad && p.err != nullptr) atomicOr(p.err, PRCR_DERR_RANGE);
       }

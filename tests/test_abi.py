@@ -41,7 +41,7 @@ def test_library_exports_every_declared_function():
     assert {"prcr_store_raw", "prcr_reassign_coords", "prcr_rebind_inject"} <= set(names)
     for n in names:
         assert hasattr(L, n), f"{n} declared in prcr.h but not exported"
-    assert L.prcr_version() == 10302
+    assert L.prcr_version() == 10303
 
 
 def test_status_strings():
@@ -89,10 +89,14 @@ def call_rebind(rope, mem, cache, total_k=10, sel_off=FAKE, sel_idx=FAKE, new_po
                                 cache_len, new_len, slots, err, None)
 
 
-def call_reassign(mem, mode=0, l_ext=2, total_k=10, new_pos=FAKE, p_txt=FAKE):
+FAR = 1 << 40          # a placeholder output address far from every input above
+
+
+def call_reassign(mem, mode=0, l_ext=2, total_k=10, new_pos=FAKE, p_txt=FAKE, next_pos=FAR,
+                  sel_off=FAKE):
     L = prcr.lib()
-    return L.prcr_reassign_coords(ctypes.byref(mem) if mem is not None else None, FAKE, FAKE,
-                                  total_k, p_txt, mode, l_ext, new_pos, FAKE, None, None)
+    return L.prcr_reassign_coords(ctypes.byref(mem) if mem is not None else None, sel_off, FAKE,
+                                  total_k, p_txt, mode, l_ext, new_pos, next_pos, None, None)
 
 
 def call_store(mem, layer=0, raw_k=FAKE, s_src=10):
@@ -177,10 +181,10 @@ def test_store_validation_errors():
 
 
 def call_revisit(rope, mem, cache, mode=0, l_ext=2, p_txt=FAKE, next_pos=FAKE + 0x200,
-                 new_pos=None, cache_len=FAKE, new_len=FAKE + 0x100):
+                 new_pos=None, cache_len=FAKE, new_len=FAKE + 0x100, sel_off=FAKE):
     L = prcr.lib()
     return L.prcr_revisit(ctypes.byref(rope), ctypes.byref(mem) if mem is not None else None,
-                          FAKE, FAKE, 10, p_txt, mode, l_ext, ctypes.byref(cache), cache_len,
+                          sel_off, FAKE, 10, p_txt, mode, l_ext, ctypes.byref(cache), cache_len,
                           new_pos, next_pos, new_len, FAKE, None, None)
 
 
@@ -198,6 +202,35 @@ def test_revisit_validation_errors():
     assert call_revisit(r2, m2, c2) == 1
     r2, m2, c2 = good(); r2.section[0], r2.section[1] = 32, 8
     assert call_revisit(r2, m2, c2) == 6
+
+
+@host_only
+def test_output_aliasing_refused():
+    # The single-launch revisit: one wave per sequence writes next_pos[b] (and the
+    # first workgroup the new lengths) while every other wave still reads p_txt,
+    # cache_len, the offsets and the visual counts.  Outputs sharing any byte with
+    # those inputs, or with each other, are refused before any HIP call.  The
+    # inputs here sit at FAKE (batch 2: 8 bytes each, 12 for the offsets).
+    rope, mem, cache = good()
+    P = FAKE + 0x400
+    assert call_revisit(rope, mem, cache, p_txt=P, next_pos=P) == 7          # in-place p_txt
+    assert call_revisit(rope, mem, cache, p_txt=P, next_pos=P + 4) == 7      # partial overlap
+    assert call_revisit(rope, mem, cache, p_txt=P, next_pos=P - 4) == 7
+    assert call_revisit(rope, mem, cache, next_pos=FAKE + 4) == 7            # cache_len, offsets
+    assert call_revisit(rope, mem, cache, p_txt=P, new_len=P) == 7           # lengths over p_txt
+    assert call_revisit(rope, mem, cache, next_pos=FAKE + 0x300, new_len=FAKE + 0x304) == 7
+    assert call_revisit(rope, mem, cache, sel_off=FAKE + 0x300, cache_len=FAKE + 0x300,
+                        p_txt=FAKE + 0x300, new_len=FAKE + 0x308) == 7      # offsets [0x300, 0x30C)
+    _, m2, _ = good(); m2.n_visual = FAKE + 0x200                           # visual counts
+    assert call_revisit(rope, m2, cache) == 7
+    # The two-call path: the lengths must not overlap the old lengths or the
+    # offsets; next_pos must not overlap the offsets or the visual counts (a
+    # workgroup reads its own p_txt[b] before writing next_pos[b], so next_pos may
+    # be p_txt there).
+    assert call_rebind(rope, mem, cache, new_len=FAKE + 4) == 7
+    assert call_rebind(rope, mem, cache, cache_len=FAKE + 0x300, new_len=FAKE + 8) == 7
+    assert call_reassign(mem, next_pos=FAKE) == 7
+    assert call_reassign(mem, sel_off=FAKE + 0x300, next_pos=FAKE + 0x308) == 7
 
 
 @host_only

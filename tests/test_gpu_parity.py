@@ -399,3 +399,52 @@ def test_special_values(dtype, paged):
     assert np.isinf(oracle.storage_to_f64(ref["k"], dtype)).any()
     exact, n = assert_parity(case, gpu, ref)
     _say(f"  keys equal to the oracle {exact}/{n}")
+
+
+INT32_MAX, INT32_MIN = 2**31 - 1, -2**31
+
+
+@pytest.mark.parametrize("fused", [False, True], ids=["two-call", "fused"])
+@pytest.mark.parametrize("mode,p_txt", [("shift", INT32_MAX - 3), ("lpa", INT32_MAX - 9),
+                                        ("pcr", INT32_MAX), ("uir", INT32_MAX)])
+def test_next_position_beyond_int32(mode, p_txt, fused):
+    """The next text position is returned as int32: a value beyond its range is
+    saturated and flagged with PRCR_DERR_RANGE, never wrapped.  Positions (double)
+    and keys follow the oracle as usual."""
+    w = workloads.make(1, "small")
+    _say(f"workload 1, mode {mode}, p_txt {p_txt}, {'fused' if fused else 'two-call'}")
+    case = Case(w)
+    pt = np.full(w.B, p_txt, np.int64)
+    gpu, ref = run_both(case, w.sel_off, w.sel_idx, pt, w.cache_len, mode=mode, fused=fused)
+    nxt = np.asarray(ref["next_pos"], np.int64)
+    over = (nxt > INT32_MAX) | (nxt < INT32_MIN)
+    assert over.all()                       # the case reaches beyond int32
+    ref["next_pos"] = np.clip(nxt, INT32_MIN, INT32_MAX)
+    ref["err"] |= prcr.DERR_RANGE
+    assert_parity(case, gpu, ref)
+
+
+def test_revisit_refuses_outputs_over_its_inputs():
+    """next_pos over p_txt (an in-place advance) or over cache_len, and new lengths
+    over p_txt, race with the other waves of the single launch: refused by the
+    binding and, called directly, by the C ABI (PRCR_ERR_ALIAS), before any launch."""
+    import ctypes
+    w = workloads.make(1, "small")
+    _say("alias refusal: workload 1, binding and C ABI")
+    case = Case(w)
+    mem, cache = case.memory(), case.cache()
+    so, si = to_dev(w.sel_off), to_dev(w.sel_idx)
+    pt, cl = to_dev(w.p_txt), to_dev(w.cache_len)
+    for kw in (dict(next_pos=pt), dict(next_pos=cl), dict(new_cache_len=pt)):
+        with pytest.raises(ValueError):
+            prcr.revisit(case.rope(), mem, so, si, pt, cache, cl, "pcr", 2, **kw)
+    L = prcr.lib()
+    slots = torch.empty(w.total_k, dtype=torch.int64, device=DEV)
+    new_len = torch.empty(w.B, dtype=torch.int32, device=DEV)
+    st = L.prcr_revisit(ctypes.byref(case.rope().to_c()), ctypes.byref(mem.to_c()),
+                        so.data_ptr(), si.data_ptr(), w.total_k, pt.data_ptr(), 0, 2,
+                        ctypes.byref(cache.to_c()), cl.data_ptr(), None, pt.data_ptr(),
+                        new_len.data_ptr(), slots.data_ptr(), None, None)
+    assert st == 7
+    torch.cuda.synchronize()
+    assert np.array_equal(pt.cpu().numpy(), w.p_txt)           # nothing was launched
