@@ -19,7 +19,9 @@
  *     are read only during the call.
  *   - Calls are asynchronous on `stream`.  The caller owns all buffers and keeps
  *     them alive until the stream work completes.  The library keeps no state
- *     between calls and allocates no memory; calls are re-entrant.
+ *     between calls and allocates no memory; calls are re-entrant.  (The one
+ *     exception is the static device scratch array of
+ *     prcr_decode_attention_static, see there.)
  *   - Structural errors (null pointer, bad shape, misalignment, unsupported
  *     combination) are detected on the host before any HIP call and returned;
  *     nothing is launched and no output is touched.  A problem too large for
@@ -82,7 +84,9 @@ typedef enum prcr_status PRCR_ENUM_BASE {
   PRCR_ERR_MODE = 5,          /* unknown reassignment mode or negative l_ext       */
   PRCR_ERR_UNSUPPORTED = 6,   /* no compiled kernel for this head_dim/axis map     */
   PRCR_ERR_ALIAS = 7,         /* an output aliases an input it must not alias      */
-  PRCR_ERR_HIP = 8            /* the HIP runtime reported a launch error           */
+  PRCR_ERR_HIP = 8,           /* the HIP runtime reported a launch error           */
+  PRCR_ERR_SCRATCH = 9        /* the call needs more than the library's static
+                                 scratch buffer (prcr_decode_attention_static)     */
 } prcr_status;
 
 typedef enum prcr_dtype PRCR_ENUM_BASE { PRCR_F32 = 0, PRCR_BF16 = 1 } prcr_dtype;
@@ -329,6 +333,38 @@ prcr_status prcr_decode_attention(const prcr_rope *rope, const prcr_cache *cache
 prcr_status prcr_decode_workspace_size(const prcr_cache *cache, int32_t batch,
                                        int32_t n_q_heads, int32_t n_kv_heads,
                                        int32_t head_dim, size_t *bytes);
+
+/* Size of the library's static device scratch buffer, per GPU. */
+#define PRCR_STATIC_SCRATCH_BYTES ((size_t)16 << 20)
+
+/*
+ * prcr_decode_attention_static - prcr_decode_attention without a caller-provided
+ * workspace, for callers that cannot allocate device memory at all (code under
+ * HIP graph capture, serving loops and harnesses that forbid hipMalloc).  It
+ * computes exactly what prcr_decode_attention computes, with the same kernels,
+ * the split-K partials going to a static device array that the library holds
+ * on every GPU it runs on (PRCR_STATIC_SCRATCH_BYTES each, from the time the
+ * library's code is loaded on that GPU until the process ends).  The call
+ * allocates nothing, on the host or the device.
+ *
+ * Arguments and errors are those of prcr_decode_attention; a shape whose
+ * partials need more than PRCR_STATIC_SCRATCH_BYTES (prcr_decode_workspace_size
+ * tells how much) returns PRCR_ERR_SCRATCH before any HIP call.  The buffer's
+ * address on the stream's GPU is looked up on the first call there (a HIP
+ * runtime failure then returns PRCR_ERR_HIP).  Every call on one GPU uses the
+ * same buffer: calls whose stream work overlaps on one GPU (different streams,
+ * or host threads racing on one stream) race on it and give undefined results;
+ * calls ordered on one stream, or separated by synchronisation, are safe.  No
+ * content is carried from one call to the next (every partial a call reads, it
+ * has written).
+ */
+prcr_status prcr_decode_attention_static(const prcr_rope *rope, const prcr_cache *cache,
+                                         prcr_dtype dtype, int32_t batch, int32_t n_layers,
+                                         int32_t n_kv_heads, int32_t layer,
+                                         const void *q, int32_t n_q_heads,
+                                         const int32_t *q_pos, const int32_t *cache_len,
+                                         float scale, float *out, int32_t *err_flag,
+                                         hipStream_t stream);
 
 /* Host helpers (no GPU work). */
 

@@ -19,7 +19,8 @@ MODES = {"pcr": 0, "shift": 1, "identity": 2, "lpa": 3, "uir": 4, "pcr_right": 5
 DERR_INDEX, DERR_CAPACITY, DERR_BLOCK, DERR_OFFSETS, DERR_RANGE = 1, 2, 4, 8, 16
 STATUS = {0: "PRCR_OK", 1: "PRCR_ERR_NULL", 2: "PRCR_ERR_SHAPE", 3: "PRCR_ERR_DTYPE",
           4: "PRCR_ERR_ALIGN", 5: "PRCR_ERR_MODE", 6: "PRCR_ERR_UNSUPPORTED",
-          7: "PRCR_ERR_ALIAS", 8: "PRCR_ERR_HIP"}
+          7: "PRCR_ERR_ALIAS", 8: "PRCR_ERR_HIP", 9: "PRCR_ERR_SCRATCH"}
+STATIC_SCRATCH_BYTES = 16 << 20     # PRCR_STATIC_SCRATCH_BYTES
 
 
 class PrcrError(RuntimeError):
@@ -88,6 +89,11 @@ def lib() -> ctypes.CDLL:
                                         c_int32, c_int32, c_void_p, c_int32, c_void_p, c_void_p,
                                         ctypes.c_float, c_void_p, c_void_p, ctypes.c_size_t, c_void_p,
                                         c_void_p]
+    L.prcr_decode_attention_static.restype = c_int
+    L.prcr_decode_attention_static.argtypes = [POINTER(CRope), POINTER(CCache), c_int, c_int32,
+                                               c_int32, c_int32, c_int32, c_void_p, c_int32,
+                                               c_void_p, c_void_p, ctypes.c_float, c_void_p,
+                                               c_void_p, c_void_p]
     L.prcr_revisit.restype = c_int
     L.prcr_revisit.argtypes = [POINTER(CRope), POINTER(CMem), c_void_p, c_void_p, c_int32, c_void_p,
                                c_int, c_int32, POINTER(CCache), c_void_p, c_void_p, c_void_p,
@@ -493,3 +499,37 @@ def decode_attention(rope: Rope, cache: Cache, layer: int, q, q_pos, cache_len, 
     _check("prcr_decode_attention", st)
     return out
 
+
+def decode_attention_static(rope: Rope, cache: Cache, layer: int, q, q_pos, cache_len, scale=None,
+                            out=None, err=None, stream=None):
+    """decode_attention whose split-K partials go to the library's static device buffer
+    (prcr_decode_attention_static): no workspace, nothing allocated by the library.
+    Calls that overlap on one GPU race on that buffer.  q [B, Hq, D] raw queries;
+    returns out float32 [B, Hq, D] (allocated here by torch when not given)."""
+    torch = _torch()
+    NL, H, D = _cache_dims(cache)
+    _need(q, "q", cache.k.dtype, 3, cache.device)
+    B, Hq = q.shape[0], q.shape[1]
+    if q.shape[2] != D:
+        raise ValueError("q head_dim differs from the cache's")
+    if cache.paged and cache.block_table.shape[0] != B:
+        raise ValueError("block_table must have one row per sequence")
+    if not cache.paged and cache.k.shape[0] != B:
+        raise ValueError("contiguous cache batch differs from q's")
+    _need(q_pos, "q_pos", torch.int32, 1, cache.device)
+    _shape(q_pos, "q_pos", (B,))
+    _need(cache_len, "cache_len", torch.int32, 1, cache.device)
+    _shape(cache_len, "cache_len", (B,))
+    if out is None:
+        out = torch.empty((B, Hq, D), dtype=torch.float32, device=cache.device)
+    _need(out, "out", torch.float32, 3, cache.device)
+    _shape(out, "out", (B, Hq, D))
+    _err(err, cache.device)
+    sc = float(D) ** -0.5 if scale is None else float(scale)
+    st = lib().prcr_decode_attention_static(ctypes.byref(rope.to_c()), ctypes.byref(cache.to_c()),
+                                            _dtype_code(cache.k), int(B), int(NL), int(H),
+                                            int(layer), _ptr(q), int(Hq), _ptr(q_pos),
+                                            _ptr(cache_len), sc, _ptr(out), _ptr(err),
+                                            _stream(stream, cache.device))
+    _check("prcr_decode_attention_static", st)
+    return out

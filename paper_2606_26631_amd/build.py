@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(PKG, "libprcr.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["api.cpp", "axis_map.cpp", "decode.hip", "prefill.hip", "reassign.hip", "rebind.hip", "store_raw.hip"]
+SOURCES = ["api.cpp", "axis_map.cpp", "decode.hip", "decode_static.hip", "prefill.hip", "reassign.hip", "rebind.hip", "store_raw.hip"]
 
 # Packed-FP32 instructions are disabled for all device code; the host pass of
 # hipcc warns that it does not know the feature, which is harmless.

@@ -11,7 +11,7 @@ using namespace prcr;
 
 namespace {
 
-constexpr int32_t kVersion = 1 * 10000 + 3 * 100 + 3;
+constexpr int32_t kVersion = 1 * 10000 + 4 * 100 + 0;
 constexpr int64_t kMaxDecodeSlots = int64_t{1} << 30;   // decode: cache capacity per sequence
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
@@ -106,6 +106,8 @@ const char *prcr_status_str(prcr_status s) {
     case PRCR_ERR_UNSUPPORTED: return "no compiled kernel for this head_dim / axis map";
     case PRCR_ERR_ALIAS: return "an output aliases an input it must not alias";
     case PRCR_ERR_HIP: return "HIP launch error";
+    case PRCR_ERR_SCRATCH:
+      return "the call needs more scratch memory than the library's static device buffer holds";
   }
   return "unknown status";
 }

@@ -41,12 +41,12 @@ def test_library_exports_every_declared_function():
     assert {"prcr_store_raw", "prcr_reassign_coords", "prcr_rebind_inject"} <= set(names)
     for n in names:
         assert hasattr(L, n), f"{n} declared in prcr.h but not exported"
-    assert L.prcr_version() == 10303
+    assert L.prcr_version() == 10400
 
 
 def test_status_strings():
     L = prcr.lib()
-    for code in range(9):
+    for code in range(10):
         assert len(L.prcr_status_str(code)) > 0
     assert L.prcr_status_str(99) == b"unknown status"
 
@@ -320,6 +320,37 @@ def test_decode_validation_errors():
     r2, _, c2 = good(); c2.paged, c2.block_table = 1, FAKE
     c2.block_size, c2.max_blocks, c2.n_blocks = 1 << 16, (1 << 14) + 1, 8
     assert call_decode(r2, c2) == 2
+
+
+def call_decode_static(rope, cache, dtype=1, batch=2, n_layers=28, n_kv=4, layer=0, q=FAKE,
+                       n_q=16, q_pos=FAKE, cache_len=FAKE, scale=0.088, out=FAKE, err=None):
+    L = prcr.lib()
+    return L.prcr_decode_attention_static(ctypes.byref(rope) if rope is not None else None,
+                                          ctypes.byref(cache) if cache is not None else None,
+                                          dtype, batch, n_layers, n_kv, layer, q, n_q, q_pos,
+                                          cache_len, scale, out, err, None)
+
+
+@host_only
+def test_decode_static_validation_errors():
+    # The same host checks as prcr_decode_attention, all before any HIP call; a
+    # shape whose split-K partials exceed the static buffer is PRCR_ERR_SCRATCH.
+    rope, _, cache = good()
+    assert call_decode_static(None, cache) == 1
+    assert call_decode_static(rope, None) == 1
+    for arg in ("q", "q_pos", "cache_len", "out"):
+        assert call_decode_static(rope, cache, **{arg: None}) == 1, arg
+    assert call_decode_static(rope, cache, dtype=5) == 3
+    assert call_decode_static(rope, cache, batch=0) == 2
+    assert call_decode_static(rope, cache, n_q=36) == 2
+    assert call_decode_static(rope, cache, layer=28) == 2
+    assert call_decode_static(rope, cache, q=FAKE + 8) == 4
+    # 65535 sequences x 32 query heads x (128 + 2) floats: about 1 GB of partials
+    n = ctypes.c_size_t(0)
+    assert prcr.lib().prcr_decode_workspace_size(ctypes.byref(cache), 65535, 32, 4, 128,
+                                                 ctypes.byref(n)) == 0
+    assert n.value > prcr.binding.STATIC_SCRATCH_BYTES
+    assert call_decode_static(rope, cache, batch=65535, n_q=32) == 9
 
 
 def test_decode_workspace_size():
