@@ -124,7 +124,7 @@ class Prepared:
                            self.cache, self.cache_len, self.new_len, self.slots, self.err, stream)
 
 
-def measure(w, steps, warmup, dev, key_only=False, mode="pcr"):
+def measure(w, steps, warmup, dev, key_only=False, mode="pcr", with_pattern=False):
     import torch
     p = Prepared(w, dev, key_only, mode)
     s = torch.cuda.Stream(device=dev)
@@ -154,36 +154,156 @@ def measure(w, steps, warmup, dev, key_only=False, mode="pcr"):
     err = int(p.err.item())
     if err != 0:
         raise RuntimeError(f"device reported data error bits {err}")
+    # The same addresses copied with no arithmetic, on the same arrays (where the
+    # arrays land in memory moves both alike), after the timed steps.
+    pattern_ms = pattern_copy(p, steps, warmup)[1] if with_pattern else None
     del p
     torch.cuda.empty_cache()
+    if with_pattern:
+        return total_ms, rebind_ms, reassign_ms, pattern_ms
     return total_ms, rebind_ms, reassign_ms
 
 
-def copy_reference(dev, nbytes=1 << 31, reps=5):
-    """A plain device-to-device copy of a known size (torch's copy kernel): the
-    attainable read+write bandwidth on this GPU, and the calibration kernel for
-    the HBM counters."""
+_COPYREF = None
+
+
+def copyref_lib():
+    """The reference copy kernels (libprcr_copyref.so, built next to libprcr.so)."""
+    global _COPYREF
+    if _COPYREF is None:
+        import ctypes
+        path = os.path.join(ROOT, "paper_2606_26631_amd", "libprcr_copyref.so")
+        if not os.path.exists(path):
+            raise ImportError(f"{path} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(path)
+        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        L.prcr_copyref_stream.restype = ctypes.c_int
+        L.prcr_copyref_stream.argtypes = [vp, vp, i64, i64, vp]
+        L.prcr_copyref_pattern.restype = ctypes.c_int
+        L.prcr_copyref_pattern.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i64, vp]
+        _COPYREF = L
+    return _COPYREF
+
+
+def _timed(fn, stream, steps, warmup):
+    """Mean and per-launch times (ms) of fn() from HIP events on `stream`."""
     import torch
-    src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        for _ in range(warmup):
+            fn()
+        evs = []
+        for _ in range(steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            evs.append((a, b))
+        torch.cuda.synchronize()
+    ms = [a.elapsed_time(b) for a, b in evs]
+    return sum(ms) / len(ms), ms
+
+
+def copy_reference(dev, nbytes=1 << 31, steps=20, warmup=3):
+    """A plain streaming copy of nbytes (each workgroup owns one contiguous 16 KB
+    chunk, 16-byte non-temporal accesses): the attainable read + write rate of this
+    GPU.  Mean of `steps` launches, as for the rebind."""
+    import torch
+    L = copyref_lib()
+    src = torch.ones(nbytes, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
     s = torch.cuda.Stream(device=dev)
-    torch.cuda.synchronize()
-    with torch.cuda.stream(s):
-        for _ in range(2):
-            dst.copy_(src)
-        ts = []
-        for _ in range(reps):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(s)
-            dst.copy_(src)
-            b.record(s)
-            ts.append((a, b))
-        torch.cuda.synchronize()
-    ms = min(a.elapsed_time(b) for a, b in ts)
+
+    def run():
+        if L.prcr_copyref_stream(src.data_ptr(), dst.data_ptr(), nbytes, 16384, s.cuda_stream) != 0:
+            raise RuntimeError("prcr_copyref_stream failed")
+
+    mean_ms, ms = _timed(run, s, steps, warmup)
+    ok = bool(torch.equal(dst[:: 1 << 20], src[:: 1 << 20]))
     del src, dst
     torch.cuda.empty_cache()
-    return {"bytes_read": nbytes, "bytes_written": nbytes,
-            "achieved": round(2 * nbytes / (ms / 1e3) / 1e9, 1), "unit": "GB/s"}
+    if not ok:
+        raise RuntimeError("the reference copy did not copy")
+    return {"kernel": "copyref stream_kernel (16 KB per workgroup)", "bytes_read": nbytes,
+            "bytes_written": nbytes, "mean_launch_us": round(mean_ms * 1e3, 2),
+            "achieved": round(2 * nbytes / (mean_ms / 1e3) / 1e9, 1), "unit": "GB/s",
+            "frac": round(2 * nbytes / (mean_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
+
+
+def rebind_rows_per_wave(total_k, rows_total, k_step=16, rows_target=72, min_waves=4096):
+    """(layer, head) rows of one token per wave in the rebinding kernel's launch for
+    bf16 / head_dim 128 (16-row load batches): about 72, in whole batches, fewer on
+    small problems so that at least 4096 waves run per array."""
+    rows_all = total_k * rows_total
+    target = rows_target
+    if rows_all < target * min_waves:
+        target = rows_all // min_waves
+    target = max(k_step, (target + k_step - 1) // k_step * k_step)
+    groups = (rows_total + target - 1) // target
+    per = (rows_total + groups - 1) // groups
+    return (per + k_step - 1) // k_step * k_step
+
+
+def pattern_offsets(w):
+    """Per-token byte offsets of the rebind's reads and writes for workload w
+    (bf16, head_dim 128): token g's first row in the memory, its row 0 in the cache,
+    and the cache's row-group rule.  Returns (src_tok, dst_tok, group_log2,
+    group_stride, rows_total, rows_per_wave)."""
+    import numpy as np
+    if w.dtype != "bf16" or w.D != 128:
+        raise ValueError("the pattern copy is built for bf16 rows of head_dim 128")
+    row = w.D * 2
+    rows_total = w.NL * w.H
+    so = np.asarray(w.sel_off, np.int64)
+    b = np.repeat(np.arange(w.B, dtype=np.int64), np.diff(so))
+    j = np.arange(w.total_k, dtype=np.int64) - so[b]
+    m = np.asarray(w.sel_idx, np.int64)
+    slot = np.asarray(w.cache_len, np.int64)[b] + j
+    src_tok = (b * w.M_max + m) * rows_total * row
+    if w.paged:
+        if w.H & (w.H - 1):
+            raise ValueError("paged pattern copy needs a power-of-two KV-head count")
+        blk = np.asarray(w.block_table, np.int64)[b, slot // w.block_size]
+        dst_tok = (blk * w.block_size + slot % w.block_size) * w.H * row
+        group_log2 = int(w.H).bit_length() - 1
+        group_stride = w.n_blocks * w.block_size * w.H * row
+    else:
+        dst_tok = (b * rows_total * w.s_max + slot) * row
+        group_log2, group_stride = 0, w.s_max * row
+    # every access stays inside the arrays
+    mem_bytes = w.B * w.M_max * rows_total * row
+    r_last = rows_total - 1
+    last_dst = (r_last >> group_log2) * group_stride + (r_last & ((1 << group_log2) - 1)) * row
+    cache_bytes = int(np.prod(workloads_cache_shape(w))) * 2
+    assert src_tok.min() >= 0 and int(src_tok.max()) + rows_total * row <= mem_bytes
+    assert dst_tok.min() >= 0 and int(dst_tok.max()) + last_dst + row <= cache_bytes
+    return (src_tok, dst_tok, group_log2, group_stride, rows_total,
+            rebind_rows_per_wave(w.total_k, rows_total))
+
+
+def workloads_cache_shape(w):
+    import workloads
+    return workloads.cache_shape(w)
+
+
+def pattern_copy(p, steps, warmup):
+    """The rebind's access pattern on the prepared arrays (memory -> cache, keys then
+    values) with no arithmetic: mean and per-launch times (ms)."""
+    import torch
+    L = copyref_lib()
+    src_tok, dst_tok, lg, gstride, rows_total, rpw = pattern_offsets(p.w)
+    dev = p.cache.k.device
+    st, dt = torch.from_numpy(src_tok).to(dev), torch.from_numpy(dst_tok).to(dev)
+    s = torch.cuda.Stream(device=dev)
+
+    def run():
+        rc = L.prcr_copyref_pattern(p.mem.k.data_ptr(), p.mem.v.data_ptr(), p.cache.k.data_ptr(),
+                                    p.cache.v.data_ptr(), st.data_ptr(), dt.data_ptr(),
+                                    p.w.total_k, rows_total, rpw, lg, gstride, s.cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"prcr_copyref_pattern failed ({rc})")
+
+    return _timed(run, s, steps, warmup)
 
 
 def small_k_latency(dev, reps=200):
@@ -525,6 +645,19 @@ def decode_attention_bw(dev, steps=20, cfg=3):
     return res
 
 
+def add_references(roof, w, pattern_ms, copy):
+    """The rebind's rate against the streaming copy and against the copy of its own
+    access pattern on the same arrays (means of the same number of launches)."""
+    mean_s = sum(pattern_ms) / len(pattern_ms) / 1e3
+    gbs = w.algorithmic_bytes() / mean_s / 1e9
+    roof["pattern_copy"] = {"kernel": "copyref pattern_kernel (the rebind's addresses, no "
+                                      "arithmetic)", "mean_launch_us": round(mean_s * 1e6, 2),
+                            "achieved": round(gbs, 1), "unit": "GB/s",
+                            "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    roof["frac_of_pattern"] = round(roof["achieved"] / gbs, 4)
+    roof["frac_of_copy"] = round(roof["achieved"] / copy["achieved"], 4)
+
+
 def roofline(w, rebind_ms, traffic):
     mean_s = sum(rebind_ms) / len(rebind_ms) / 1e3
     gbs = w.algorithmic_bytes() / mean_s / 1e9
@@ -597,34 +730,49 @@ def _oracle_worker(args):
     return _oracle_loop(w, first, budget_s)
 
 
+def cpu_model() -> str:
+    """The host CPU's model name, from /proc/cpuinfo."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, budget_s=10.0):
     """The oracle, as it stands, on whole sequences of workload w (one sequence per
     call: reassignment + rebind/inject into that sequence's cache), timed on the
-    host before any GPU work: in this process (1 thread), then in a pool of worker
-    processes, one per available core (up to 16), each for about budget_s seconds.
-    Inputs are built on the host, untimed."""
+    host before any GPU work: in a pool of worker processes, one per core available
+    to this process (at most 16, the host CPU share of one GPU on these machines),
+    each for about budget_s seconds and each starting at a different sequence;
+    then in this process alone (1 thread).  Inputs (up to 8 sequences, about 7.5
+    GB) are built on the host, untimed."""
     import multiprocessing as mp
-    _CPU_INPUTS[:] = _cpu_inputs(w)
+    _CPU_INPUTS[:] = _cpu_inputs(w, max_bytes=7 << 30)
     n_seq = len(_CPU_INPUTS)
-    done, spent, calls = _oracle_loop(w, 0, budget_s)
-    one = {"value": round(done / spent, 1), "unit": "entries/s", "cores": 1, "kind": "oracle",
-           "sample": f"{calls} oracle calls, one sequence of workload {w.cfg} each (sequences "
-                     f"0..{n_seq - 1} in turn): {done} entries in {spent:.1f} s, numpy float64, "
-                     "1 thread"}
-    workers = max(1, min(16, len(os.sched_getaffinity(0))))
+    avail = len(os.sched_getaffinity(0))
+    workers = max(1, min(16, avail))
     t = time.perf_counter()
     with mp.get_context("fork").Pool(workers) as pool:
         res = pool.map(_oracle_worker, [(w, i, budget_s) for i in range(workers)])
     wall = time.perf_counter() - t
     done_all = sum(r[0] for r in res)
-    one["all_cores"] = {
-        "value": round(done_all / wall, 1), "unit": "entries/s", "cores": workers,
-        "kind": "oracle",
-        "sample": f"{workers} worker processes, one per core, each running oracle calls on the "
-                  f"same {n_seq} sequences for about {budget_s:.0f} s: {done_all} entries in "
-                  f"{wall:.1f} s wall time"}
+    out = {"value": round(done_all / wall, 1), "unit": "entries/s", "cores": workers,
+           "kind": "oracle", "cpu_model": cpu_model(), "cores_available": avail,
+           "sample": f"workload {w.cfg}: {workers} worker processes (one per core), each "
+                     f"running whole-sequence oracle calls (reassignment + rebind/inject) over "
+                     f"sequences 0..{n_seq - 1} round robin from its own start for about "
+                     f"{budget_s:.0f} s: {done_all} entries in {wall:.1f} s wall time, numpy "
+                     "float64, one thread per process"}
+    done, spent, calls = _oracle_loop(w, 0, budget_s)
+    out["one_core"] = {"value": round(done / spent, 1), "unit": "entries/s", "cores": 1,
+                       "sample": f"{calls} oracle calls in this process, sequences "
+                                 f"0..{n_seq - 1} in turn: {done} entries in {spent:.1f} s"}
     _CPU_INPUTS.clear()
-    return one
+    return out
 
 
 def main():
@@ -662,7 +810,8 @@ def main():
     import torch
     dev = torch.device("cuda:0")
     khash = kernel_source_hash()
-    total_ms, rebind_ms, reassign_ms = measure(w, args.steps, args.warmup, dev)
+    total_ms, rebind_ms, reassign_ms, pattern_ms = measure(w, args.steps, args.warmup, dev,
+                                                           with_pattern=True)
     ms_step = total_ms / args.steps
     out = {
         "metric": "rebound KV entries/sec (layers\u00d7heads\u00d7tokens) and achieved HBM GB/s vs peak",
@@ -677,16 +826,15 @@ def main():
     }
     copy = copy_reference(dev)
     out["attainable_copy"] = copy
-    out["roofline"]["frac_of_copy"] = round(out["roofline"]["achieved"] / copy["achieved"], 4)
+    add_references(out["roofline"], w, pattern_ms, copy)
     if args.secondary:
         w2 = workloads.make(args.secondary, "full")
-        t2, r2, a2 = measure(w2, args.steps, args.warmup, dev)
+        t2, r2, a2, p2 = measure(w2, args.steps, args.warmup, dev, with_pattern=True)
         out["secondary"] = {"config": describe(w2),
                             "value": round(w2.entries() * args.steps / (t2 / 1e3), 1),
                             "unit": "entries/s", "ms_per_step": round(t2 / args.steps, 4),
                             "roofline": roofline(w2, r2, load_traffic(f"rebind_workload{w2.cfg}", "rebind"))}
-        out["secondary"]["roofline"]["frac_of_copy"] = round(
-            out["secondary"]["roofline"]["achieved"] / copy["achieved"], 4)
+        add_references(out["secondary"]["roofline"], w2, p2, copy)
     def key_only():
         wk = workloads.make(args.workload, "full")
         _, rk, _ = measure(wk, args.steps, args.warmup, dev, key_only=True)

@@ -19,6 +19,11 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(PKG, "libprcr.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
+# The bandwidth measurement's reference copies (a plain streaming copy and a copy
+# with the rebinding kernel's access pattern), in a library of their own: they are
+# not part of the PRCR path or its ABI.
+COPYREF_SOURCES = ["copyref.hip"]
+COPYREF_OUT = os.path.join(PKG, "libprcr_copyref.so")
 SOURCES = ["api.cpp", "axis_map.cpp", "decode.hip", "decode_static.hip", "prefill.hip", "reassign.hip", "rebind.hip", "store_raw.hip"]
 
 # Packed-FP32 instructions are disabled for all device code; the host pass of
@@ -49,19 +54,25 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source for gfx950 and link libprcr.so; returns its path."""
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = OUT + ".tmp"
+def _link(objs, out: str, verbose: bool) -> None:
+    tmp = out + ".tmp"
     cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, OUT)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source for gfx950 and link libprcr.so, and the measurement's
+    reference copy kernels into libprcr_copyref.so; returns libprcr.so's path."""
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES) + len(COPYREF_SOURCES))) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES + COPYREF_SOURCES))
+    _link(objs[:len(SOURCES)], OUT, verbose)
+    _link(objs[len(SOURCES):], COPYREF_OUT, verbose)
     return OUT
 
 
