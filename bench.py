@@ -179,6 +179,8 @@ def copyref_lib():
         vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
         L.prcr_copyref_stream.restype = ctypes.c_int
         L.prcr_copyref_stream.argtypes = [vp, vp, i64, i64, vp]
+        L.prcr_copyref_decode_read.restype = ctypes.c_int
+        L.prcr_copyref_decode_read.argtypes = [vp, vp, vp, vp, vp] + [i32] * 10 + [vp]
         L.prcr_copyref_pattern.restype = ctypes.c_int
         L.prcr_copyref_pattern.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i64, vp]
         _COPYREF = L
@@ -636,7 +638,26 @@ def decode_attention_bw(dev, steps=20, cfg=3):
     ms = [a.elapsed_time(b) for a, b in evs]
     mean_s = sum(ms) / len(ms) / 1e3
     nbytes = int(lens.sum()) * w.H * w.D * 2 * 2 + w.B * Hq * w.D * (2 + 4)
-    del cache, ws
+    # The same K and V reads with no arithmetic (copyref decode_read_kernel), on the
+    # same cache, with the decode kernel's split and lane layout.
+    L = copyref_lib()
+    per_split = w.B * Hq * (w.D + 2) * 4
+    n_split = prcr.decode_workspace_bytes(cache, w.B, Hq) // per_split
+    sink = torch.empty(w.B * w.H * n_split, dtype=torch.int32, device=dev)
+    cc = cache.to_c()
+
+    def read_pattern():
+        rc = L.prcr_copyref_decode_read(cache.k.data_ptr(), cache.v.data_ptr(),
+                                        cache.block_table.data_ptr() if w.paged else None,
+                                        cl.data_ptr(), sink.data_ptr(), w.B, w.NL, w.H, 0,
+                                        cc.s_max, cc.block_size, cc.max_blocks, cc.n_blocks,
+                                        n_split, int(w.paged), s.cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"prcr_copyref_decode_read failed ({rc})")
+
+    read_ms, _ = _timed(read_pattern, s, steps, 3)
+    read_bytes = int(lens.sum()) * w.H * w.D * 2 * 2
+    del cache, ws, sink
     torch.cuda.empty_cache()
     layout = f"paged, block {w.block_size}" if w.paged else "contiguous"
     res = {"kernel": "prcr_decode_attention", "workload": f"workload {cfg}: {w.B} sequences, cache "
@@ -644,6 +665,12 @@ def decode_attention_bw(dev, steps=20, cfg=3):
            f"bf16, {layout}, one layer per call", "mean_call_us": round(mean_s * 1e6, 2),
            "algorithmic_bytes_per_call": nbytes, "achieved": round(nbytes / mean_s / 1e9, 1),
            "unit": "GB/s", "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4)}
+    read_gbs = read_bytes / (read_ms / 1e3) / 1e9
+    res["pattern_read"] = {"kernel": "copyref decode_read_kernel (the same K/V reads, no "
+                                     "arithmetic)", "mean_launch_us": round(read_ms * 1e3, 2),
+                           "bytes": read_bytes, "achieved": round(read_gbs, 1), "unit": "GB/s",
+                           "frac": round(read_gbs / HBM_PEAK_GBS, 4)}
+    res["frac_of_pattern"] = round(res["achieved"] / read_gbs, 4)
     res["traffic"] = load_traffic("decode_attention" if cfg == 3 else "decode_attention_paged",
                                   "decode")
     return res

@@ -4,6 +4,11 @@
 //
 //   prcr_copyref_stream   src -> dst, each workgroup owning one contiguous chunk:
 //                         the attainable read + write rate of the GPU.
+//   prcr_copyref_decode_read  decode attention's reads with no arithmetic: every K and
+//                         V row of one layer's attended slots, with the decode
+//                         kernel's split of each sequence over workgroups, lane
+//                         layout (16 lanes per 256-byte row) and two rows per lane
+//                         group in flight.
 //   prcr_copyref_pattern  the rebind's own access pattern with no arithmetic and no
 //                         metadata: per selected token, its (layer, head) rows are
 //                         read from one contiguous run of the memory and written to
@@ -129,6 +134,80 @@ __global__ __launch_bounds__(kThreads) void pattern_kernel(const PatternParams p
   }
 }
 
+struct DecodeReadParams {
+  const char *k;               // cache keys
+  const char *v;               // cache values
+  const int32_t *block_table;  // paged: [batch][max_blocks]
+  const int32_t *len;          // [batch] attended slots
+  uint32_t *out;               // [gridDim.z][gridDim.y][gridDim.x] one word per workgroup
+  int32_t n_layers, n_kv_heads, layer, s_max, block_size, max_blocks, n_blocks, n_split, paged;
+};
+
+// One workgroup per (split, KV head, sequence), as the decode kernel launches them.
+// Rows are 256 bytes (head_dim 128, bf16): 16 lanes per row, 4 rows per wave and
+// 16 per workgroup per pass, two passes' rows in flight, loads of a batch issued
+// unconditionally (a row past the chunk reads the head's first row, as in the
+// decode kernel).  The words read are folded into one value per workgroup so that
+// the loads are kept.
+__global__ __launch_bounds__(kThreads) void decode_read_kernel(const DecodeReadParams p) {
+  constexpr int kRowBytes = 256, kLanesPerRow = 16, kRowsPerWg = 16, kIters = 2;
+  const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int grp = wave * (64 / kLanesPerRow) + lane / kLanesPerRow;
+  const int c = lane % kLanesPerRow;
+  const int len = p.len[b];
+  const int per = (len + p.n_split - 1) / p.n_split;
+  const int chunk = (per + kRowsPerWg - 1) / kRowsPerWg * kRowsPerWg;
+  const int j0 = min(len, split * chunk), j1 = min(len, j0 + chunk);
+  const int64_t row_base =
+      p.paged ? 0 : ((static_cast<int64_t>(b) * p.n_layers + p.layer) * p.n_kv_heads + kvh) * p.s_max;
+  const int64_t row_any =
+      p.paged ? static_cast<int64_t>(p.layer) * p.n_blocks * p.block_size * p.n_kv_heads + kvh : row_base;
+  uint32_t acc = 0;
+  auto load = [&](int jb, u32x4 *kd, u32x4 *vd) {
+    int64_t rows[kIters];
+#pragma unroll
+    for (int u = 0; u < kIters; ++u) {
+      const int j = jb + u * kRowsPerWg + grp;
+      int64_t row = row_base + j;
+      if (p.paged) {
+        const int js = j < j1 ? j : 0;
+        const int lb = js / p.block_size;
+        const int blk = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
+        row = ((static_cast<int64_t>(p.layer) * p.n_blocks + blk) * p.block_size + (js - lb * p.block_size)) *
+                  p.n_kv_heads + kvh;
+      }
+      rows[u] = j < j1 ? row : row_any;
+    }
+#pragma unroll
+    for (int u = 0; u < kIters; ++u) {
+      kd[u] = ld(p.k + rows[u] * kRowBytes + c * 16);
+      vd[u] = ld(p.v + rows[u] * kRowBytes + c * 16);
+    }
+  };
+  u32x4 kc[kIters], vc[kIters];
+  load(j0, kc, vc);
+  for (int jb = j0; jb < j1; jb += kRowsPerWg * kIters) {
+    u32x4 nk[kIters], nv[kIters];
+    load(jb + kRowsPerWg * kIters, nk, nv);
+#pragma unroll
+    for (int u = 0; u < kIters; ++u) {
+      acc ^= kc[u].x ^ kc[u].y ^ kc[u].z ^ kc[u].w ^ vc[u].x ^ vc[u].y ^ vc[u].z ^ vc[u].w;
+      kc[u] = nk[u];
+      vc[u] = nv[u];
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) acc ^= __shfl_xor(acc, o);
+  __shared__ uint32_t s_acc[kThreads / 64];
+  if (lane == 0) s_acc[wave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t a = 0;
+    for (int w = 0; w < kThreads / 64; ++w) a ^= s_acc[w];
+    p.out[(static_cast<int64_t>(b) * gridDim.y + kvh) * gridDim.x + split] = a;
+  }
+}
+
 }  // namespace
 
 extern "C" {
@@ -171,6 +250,36 @@ int prcr_copyref_pattern(const void *src_k, const void *src_v, void *dst_k, void
   const int64_t grid = (static_cast<int64_t>(n_tok) + 3) / 4 * p.n_row_groups * 2;
   if (grid > 0x7FFFFFFF / kThreads) return 2;
   pattern_kernel<<<dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0, stream>>>(p);
+  return hipGetLastError() == hipSuccess ? 0 : 3;
+}
+
+// Decode attention's reads of one layer (see above): n_split workgroups per
+// (sequence, KV head); out holds batch * n_kv_heads * n_split words.
+int prcr_copyref_decode_read(const void *k, const void *v, const int32_t *block_table,
+                             const int32_t *len, uint32_t *out, int32_t batch, int32_t n_layers,
+                             int32_t n_kv_heads, int32_t layer, int32_t s_max, int32_t block_size,
+                             int32_t max_blocks, int32_t n_blocks, int32_t n_split, int32_t paged,
+                             hipStream_t stream) {
+  if (k == nullptr || v == nullptr || len == nullptr || out == nullptr || batch < 1 ||
+      batch > 65535 || n_kv_heads < 1 || n_kv_heads > 65535 || n_split < 1 || layer < 0 ||
+      layer >= n_layers || (paged && (block_table == nullptr || block_size < 1)))
+    return 1;
+  DecodeReadParams p{};
+  p.k = static_cast<const char *>(k);
+  p.v = static_cast<const char *>(v);
+  p.block_table = block_table;
+  p.len = len;
+  p.out = out;
+  p.n_layers = n_layers;
+  p.n_kv_heads = n_kv_heads;
+  p.layer = layer;
+  p.s_max = s_max;
+  p.block_size = block_size;
+  p.max_blocks = max_blocks;
+  p.n_blocks = n_blocks;
+  p.n_split = n_split;
+  p.paged = paged;
+  decode_read_kernel<<<dim3(n_split, n_kv_heads, batch), dim3(kThreads), 0, stream>>>(p);
   return hipGetLastError() == hipSuccess ? 0 : 3;
 }
 

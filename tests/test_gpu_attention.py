@@ -73,6 +73,42 @@ def test_decode_attention_parity(dtype, D, G, paged):
     assert not out[0].any()
 
 
+# Paged pools whose KV-head count is a multiple of 4 take the head-per-wave
+# mapping (a workgroup's waves on the heads of the same slots): every head checked.
+HEAD_WAVE_CASES = [("bf16", 128, 4, 4, 16), ("bf16", 128, 2, 8, 16), ("f32", 64, 1, 4, 5),
+                   ("bf16", 64, 8, 4, 1), ("bf16", 128, 3, 12, 16), ("f32", 128, 4, 8, 7)]
+
+
+@pytest.mark.parametrize("dtype,D,G,H,bs", HEAD_WAVE_CASES)
+def test_decode_attention_parity_paged_head_waves(dtype, D, G, H, bs):
+    B, NL, layer = 4, 2, 1
+    lens = np.array([0, 1, 700, 333], np.int32)
+    cap = 800
+    g = torch.Generator().manual_seed(100 + D + G + H)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    rnd = lambda *s: torch.randn(s, generator=g).to(tdt)
+    rng = np.random.default_rng(H * 10 + G)
+    need = (cap + bs - 1) // bs
+    table = rng.permutation(B * need + 3)[:B * need].astype(np.int32).reshape(B, need)
+    k, v = rnd(NL, B * need + 3, bs, H, D), rnd(NL, B * need + 3, bs, H, D)
+    cache_o = {"paged": True, "block_size": bs, "block_table": table, "max_blocks": need,
+               "n_blocks": B * need + 3}
+    cache_o["k"], cache_o["v"] = workloads.as_numpy_storage(k), workloads.as_numpy_storage(v)
+    q = rnd(B, H * G, D)
+    q_pos = rng.integers(0, 20000, B).astype(np.int32)
+    _say(f"decode attention paged head-per-wave {dtype} D={D} G={G} H={H} block {bs}")
+    cache = prcr.Cache(k.to(DEV), v.to(DEV), to_dev(table))
+    rope = prcr.Rope(D, (8, 12, 12) if D == 64 else (16, 24, 24), False, 1e6)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out = prcr.decode_attention(rope, cache, layer, q.to(DEV), to_dev(q_pos), to_dev(lens), err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    ref = oracle.decode_attention(rope.__dict__ | {"sections": rope.sections}, cache_o, layer,
+                                  workloads.as_numpy_storage(q), q_pos, lens, D ** -0.5, dtype)
+    _check(out, ref, cache_o, lens, H, G, dtype, layer)
+    assert not out[0].any()
+
+
 def test_decode_after_prefill_and_revisit():
     """The path end to end on the GPU against the oracle: every layer's prefill
     capture, a PCR revisit of selected visual tokens, then decode attention of the

@@ -67,7 +67,7 @@ def test_random_decode_configuration(seed):
     D = int(r.choice([64, 128]))
     sections, inter = MAPS[D][int(r.integers(len(MAPS[D])))]
     dtype = str(r.choice(["f32", "bf16"]))
-    B, H, G, NL = int(r.integers(1, 6)), int(r.integers(1, 4)), int(r.choice([1, 2, 3, 4, 7, 8])), 2
+    B, H, G, NL = int(r.integers(1, 6)), int(r.choice([1, 2, 3, 4, 8])), int(r.choice([1, 2, 3, 4, 7, 8])), 2
     layer = int(r.integers(NL))
     cap = int(r.integers(1, 400))
     lens = r.integers(0, cap + 1, B).astype(np.int32)
