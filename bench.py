@@ -181,6 +181,8 @@ def copyref_lib():
         L.prcr_copyref_stream.argtypes = [vp, vp, i64, i64, vp]
         L.prcr_copyref_decode_read.restype = ctypes.c_int
         L.prcr_copyref_decode_read.argtypes = [vp, vp, vp, vp, vp] + [i32] * 10 + [vp]
+        L.prcr_copyref_prefill.restype = ctypes.c_int
+        L.prcr_copyref_prefill.argtypes = [vp] * 8 + [i32] * 7 + [vp]
         L.prcr_copyref_pattern.restype = ctypes.c_int
         L.prcr_copyref_pattern.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i64, vp]
         _COPYREF = L
@@ -425,6 +427,21 @@ def prefill_capture_bw(dev, steps=20, NL=36, H=8):
     rows = int(n_tok.sum()) * H
     vrows = int(n_vis.sum()) * H
     nbytes = (rows * 2 * 2 + vrows * 2) * D * 2
+    # The same reads and writes with no arithmetic (copyref prefill_pattern_kernel),
+    # on the same arrays, with the prefill kernel's wave mapping.
+    L = copyref_lib()
+    state = {"i": 0}
+
+    def pattern():
+        rc = L.prcr_copyref_prefill(raw_k.data_ptr(), raw_v.data_ptr(), args[2].data_ptr(),
+                                    args[1].data_ptr(), cache.k.data_ptr(), cache.v.data_ptr(),
+                                    mem.k.data_ptr(), mem.v.data_ptr(), B, S, H, NL,
+                                    state["i"] % NL, s_max, M, s.cuda_stream)
+        state["i"] += 1
+        if rc != 0:
+            raise RuntimeError(f"prcr_copyref_prefill failed ({rc})")
+
+    pat_ms, _ = _timed(pattern, s, steps, 3)
     del mem, cache, raw_k, raw_v
     torch.cuda.empty_cache()
     return {"kernel": "prcr_prefill_capture", "workload": f"{B} prompts x {S} tokens "
@@ -432,6 +449,11 @@ def prefill_capture_bw(dev, steps=20, NL=36, H=8):
             "mean_launch_us": round(mean_s * 1e6, 2), "algorithmic_bytes_per_call": nbytes,
             "achieved": round(nbytes / mean_s / 1e9, 1), "unit": "GB/s",
             "frac": round(nbytes / mean_s / 1e9 / HBM_PEAK_GBS, 4),
+            "pattern_copy": {"kernel": "copyref prefill_pattern_kernel (the same reads and writes, no "
+                                       "arithmetic)", "mean_launch_us": round(pat_ms * 1e3, 2),
+                             "achieved": round(nbytes / (pat_ms / 1e3) / 1e9, 1), "unit": "GB/s",
+                             "frac": round(nbytes / (pat_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)},
+            "frac_of_pattern": round(pat_ms / 1e3 / mean_s, 4),
             "traffic": load_traffic("prefill_capture" if H == 8 else f"prefill_capture_{H}kv", "prefill")}
 
 

@@ -9,6 +9,12 @@
 //                         kernel's split of each sequence over workgroups, lane
 //                         layout (16 lanes per 256-byte row) and two rows per lane
 //                         group in flight.
+//   prcr_copyref_prefill  prefill capture's access pattern with no arithmetic: one
+//                         layer's raw K/V rows of every prompt token to the
+//                         contiguous cache at slot s, and visual tokens' rows to the
+//                         memory, with the prefill kernel's wave mapping (8
+//                         consecutive (token, head) rows per wave, lane layout as
+//                         in the rebind).
 //   prcr_copyref_pattern  the rebind's own access pattern with no arithmetic and no
 //                         metadata: per selected token, its (layer, head) rows are
 //                         read from one contiguous run of the memory and written to
@@ -208,6 +214,48 @@ __global__ __launch_bounds__(kThreads) void decode_read_kernel(const DecodeReadP
   }
 }
 
+struct PrefillPatternParams {
+  const char *raw_k, *raw_v;   // [batch][s_src][H][128] bf16 rows
+  const int32_t *vis_index;    // [batch][s_src]: visual index or -1
+  const int32_t *n_tokens;     // [batch]
+  char *cache_k, *cache_v;     // contiguous [batch][n_layers][H][s_max][128]
+  char *mem_k, *mem_v;         // [batch][max_visual][n_layers][H][128]
+  int32_t batch, s_src, n_kv_heads, n_layers, layer, s_max, max_visual;
+};
+
+// Rows are 256 bytes (head_dim 128, bf16); row R = (b * s_src + s) * H + h.
+__global__ __launch_bounds__(kThreads) void prefill_pattern_kernel(const PrefillPatternParams p) {
+  constexpr int kRowBytes = 256, kHalf = 128, kLanesPerRow = 8, kRowsPerWave = 8;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int H = p.n_kv_heads;
+  const int64_t rows_all = static_cast<int64_t>(p.batch) * p.s_src * H;
+  const int64_t R = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * kRowsPerWave + lane / kLanesPerRow;
+  if (R >= rows_all) return;
+  const int c = lane % kLanesPerRow;
+  const int b = static_cast<int>(R / (static_cast<int64_t>(p.s_src) * H));
+  const int64_t rem = R - static_cast<int64_t>(b) * p.s_src * H;
+  const int s = static_cast<int>(rem / H), h = static_cast<int>(rem - static_cast<int64_t>(s) * H);
+  const int nt = p.n_tokens[b];
+  const int m = p.vis_index[static_cast<int64_t>(b) * p.s_src + s];
+  if (s >= nt || s >= p.s_max) return;
+  const int64_t o = R * kRowBytes + c * 16;
+  const u32x4 kl = ld(p.raw_k + o), kh = ld(p.raw_k + o + kHalf);
+  const u32x4 vl = ld(p.raw_v + o), vh = ld(p.raw_v + o + kHalf);
+  const int64_t d = ((((static_cast<int64_t>(b) * p.n_layers + p.layer) * H + h) * p.s_max) + s) * kRowBytes + c * 16;
+  st(p.cache_k + d, kl);
+  st(p.cache_k + d + kHalf, kh);
+  st(p.cache_v + d, vl);
+  st(p.cache_v + d + kHalf, vh);
+  if (m >= 0 && m < p.max_visual) {
+    const int64_t mo = (((static_cast<int64_t>(b) * p.max_visual + m) * p.n_layers + p.layer) * H + h) * kRowBytes +
+                       c * 16;
+    st(p.mem_k + mo, kl);
+    st(p.mem_k + mo + kHalf, kh);
+    st(p.mem_v + mo, vl);
+    st(p.mem_v + mo + kHalf, vh);
+  }
+}
+
 }  // namespace
 
 extern "C" {
@@ -280,6 +328,40 @@ int prcr_copyref_decode_read(const void *k, const void *v, const int32_t *block_
   p.n_split = n_split;
   p.paged = paged;
   decode_read_kernel<<<dim3(n_split, n_kv_heads, batch), dim3(kThreads), 0, stream>>>(p);
+  return hipGetLastError() == hipSuccess ? 0 : 3;
+}
+
+// Prefill capture's access pattern for one layer (see above).
+int prcr_copyref_prefill(const void *raw_k, const void *raw_v, const int32_t *vis_index,
+                         const int32_t *n_tokens, void *cache_k, void *cache_v, void *mem_k,
+                         void *mem_v, int32_t batch, int32_t s_src, int32_t n_kv_heads,
+                         int32_t n_layers, int32_t layer, int32_t s_max, int32_t max_visual,
+                         hipStream_t stream) {
+  if (raw_k == nullptr || raw_v == nullptr || vis_index == nullptr || n_tokens == nullptr ||
+      cache_k == nullptr || cache_v == nullptr || mem_k == nullptr || mem_v == nullptr ||
+      batch < 1 || s_src < 1 || n_kv_heads < 1 || layer < 0 || layer >= n_layers || s_max < 1 ||
+      max_visual < 1)
+    return 1;
+  PrefillPatternParams p{};
+  p.raw_k = static_cast<const char *>(raw_k);
+  p.raw_v = static_cast<const char *>(raw_v);
+  p.vis_index = vis_index;
+  p.n_tokens = n_tokens;
+  p.cache_k = static_cast<char *>(cache_k);
+  p.cache_v = static_cast<char *>(cache_v);
+  p.mem_k = static_cast<char *>(mem_k);
+  p.mem_v = static_cast<char *>(mem_v);
+  p.batch = batch;
+  p.s_src = s_src;
+  p.n_kv_heads = n_kv_heads;
+  p.n_layers = n_layers;
+  p.layer = layer;
+  p.s_max = s_max;
+  p.max_visual = max_visual;
+  const int64_t rows = static_cast<int64_t>(batch) * s_src * n_kv_heads;
+  const int64_t grid = (rows + 31) / 32;
+  if (grid > 0x7FFFFFFF / kThreads) return 2;
+  prefill_pattern_kernel<<<dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0, stream>>>(p);
   return hipGetLastError() == hipSuccess ? 0 : 3;
 }
 

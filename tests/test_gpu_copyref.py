@@ -59,3 +59,40 @@ def test_stream_copy_copies():
                                  torch.cuda.current_stream().cuda_stream) == 0
     torch.cuda.synchronize()
     assert torch.equal(src, dst)
+
+
+def test_prefill_pattern_copy_writes_the_prefills_rows():
+    """The prefill pattern copy writes every prompt row raw into the cache slot the
+    prefill uses (slot s of a contiguous cache) and every visual row into the memory,
+    and nothing else."""
+    B, NL, H, D, layer = 2, 3, 4, 128, 1
+    pos, vis, n_tok, n_vis = workloads.prompt(B, n_before=(5, 9), grid=((4, 6), (3, 5)),
+                                              n_after=(3, 0), frames=(1, 2))
+    S, M = pos.shape[1], int(n_vis.max())
+    print(f"prefill pattern copy: B={B} S={S} M={M} H={H}", flush=True)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(77)
+    raw_k = torch.randn((B, S, H, D), generator=g, device=DEV).to(torch.bfloat16)
+    raw_v = torch.randn((B, S, H, D), generator=g, device=DEV).to(torch.bfloat16)
+    ck = torch.randn((B, NL, H, S + 4, D), generator=g, device=DEV).to(torch.bfloat16)
+    cv, mk, mv = ck.clone() + 1, torch.randn((B, M, NL, H, D), generator=g, device=DEV).to(
+        torch.bfloat16), None
+    mv = mk.clone() + 1
+    before = [x.clone() for x in (ck, cv, mk, mv)]
+    L = bench.copyref_lib()
+    assert L.prcr_copyref_prefill(raw_k.data_ptr(), raw_v.data_ptr(), to_dev(vis).data_ptr(),
+                                  to_dev(n_tok).data_ptr(), ck.data_ptr(), cv.data_ptr(),
+                                  mk.data_ptr(), mv.data_ptr(), B, S, H, NL, layer, S + 4, M,
+                                  torch.cuda.current_stream().cuda_stream) == 0
+    torch.cuda.synchronize()
+    exp = [x.clone() for x in before]
+    for b in range(B):
+        for s in range(int(n_tok[b])):
+            exp[0][b, layer, :, s] = raw_k[b, s]
+            exp[1][b, layer, :, s] = raw_v[b, s]
+            m = int(vis[b, s])
+            if m >= 0:
+                exp[2][b, m, layer] = raw_k[b, s]
+                exp[3][b, m, layer] = raw_v[b, s]
+    for got, want in zip((ck, cv, mk, mv), exp):
+        assert torch.equal(got, want)
