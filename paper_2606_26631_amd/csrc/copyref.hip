@@ -161,7 +161,11 @@ __global__ __launch_bounds__(kThreads) void decode_read_kernel(const DecodeReadP
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = wave * (64 / kLanesPerRow) + lane / kLanesPerRow;
   const int c = lane % kLanesPerRow;
-  const int len = p.len[b];
+  // lengths clamped to the capacity, and block-table entries outside the pool
+  // read the head's first row instead, as in the decode kernel: every access stays
+  // inside the arrays whatever the inputs
+  const int64_t cap = p.paged ? static_cast<int64_t>(p.max_blocks) * p.block_size : p.s_max;
+  const int len = static_cast<int>(min(max(static_cast<int64_t>(p.len[b]), int64_t{0}), cap));
   const int per = (len + p.n_split - 1) / p.n_split;
   const int chunk = (per + kRowsPerWg - 1) / kRowsPerWg * kRowsPerWg;
   const int j0 = min(len, split * chunk), j1 = min(len, j0 + chunk);
@@ -180,8 +184,10 @@ __global__ __launch_bounds__(kThreads) void decode_read_kernel(const DecodeReadP
         const int js = j < j1 ? j : 0;
         const int lb = js / p.block_size;
         const int blk = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
-        row = ((static_cast<int64_t>(p.layer) * p.n_blocks + blk) * p.block_size + (js - lb * p.block_size)) *
-                  p.n_kv_heads + kvh;
+        row = blk >= 0 && blk < p.n_blocks
+                  ? ((static_cast<int64_t>(p.layer) * p.n_blocks + blk) * p.block_size +
+                     (js - lb * p.block_size)) * p.n_kv_heads + kvh
+                  : row_any;
       }
       rows[u] = j < j1 ? row : row_any;
     }
@@ -310,7 +316,8 @@ int prcr_copyref_decode_read(const void *k, const void *v, const int32_t *block_
                              hipStream_t stream) {
   if (k == nullptr || v == nullptr || len == nullptr || out == nullptr || batch < 1 ||
       batch > 65535 || n_kv_heads < 1 || n_kv_heads > 65535 || n_split < 1 || layer < 0 ||
-      layer >= n_layers || (paged && (block_table == nullptr || block_size < 1)))
+      layer >= n_layers || (paged && (block_table == nullptr || block_size < 1 || max_blocks < 1 ||
+                                      n_blocks < 1)) || (!paged && s_max < 1))
     return 1;
   DecodeReadParams p{};
   p.k = static_cast<const char *>(k);
