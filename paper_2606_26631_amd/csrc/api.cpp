@@ -355,7 +355,7 @@ static prcr_status decode_shape(const prcr_cache *cache, int32_t batch, int32_t 
   }
   // Slot indices, plus a few batches of look-ahead, stay far inside 32 bits.
   if (cap > kMaxDecodeSlots) return PRCR_ERR_SHAPE;
-  *n_split = decode_splits(cap, batch, n_kv_heads);
+  *n_split = decode_splits(cap, batch, n_kv_heads, n_q_heads / n_kv_heads);
   return PRCR_OK;
 }
 

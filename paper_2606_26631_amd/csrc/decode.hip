@@ -6,16 +6,19 @@
 //
 // Split-K flash decoding.  Kernel 1: one workgroup per (key chunk, KV head,
 // sequence) streams its keys and values once for all G query heads of the
-// group: a 16-byte chunk of a key row per lane, scores reduced across the lanes
-// of a row with DPP lane permutations, online softmax in float32 with one
-// rescale per batch of rows, and only when a running maximum rose.  The
-// sequence's keys are split evenly over its workgroups.  The workgroup's key
-// groups are merged in LDS and one (max, sum, weighted V) partial per query
-// head and chunk is written to the caller's workspace.  Kernel 2 merges the
-// chunks.
+// group, and the sequence's keys are split evenly over its workgroups, about as
+// many workgroups in all as the chip holds at once.  bf16 caches take the
+// scores of 16 keys at a time from matrix-core products (decode_partial_bf16_kernel);
+// float32 caches take a 16-byte chunk of a key row per lane with scores reduced
+// across the lanes of a row by DPP lane permutations (decode_partial_kernel).
+// Both keep an online softmax in float32 that rescales only when a running
+// maximum rose.  The workgroup's waves are merged in LDS and one (max, sum,
+// weighted V) partial per query head and chunk is written to the caller's
+// workspace.  Kernel 2 merges the chunks.
 #include <cfloat>
 #include <climits>
 #include <cmath>
+#include <type_traits>
 
 #include "prcr_internal.h"
 #include "rotary.h"
@@ -27,7 +30,10 @@ namespace {
 #define PRCR_DEC_ITERS 2
 #endif
 #ifndef PRCR_DEC_WORKGROUPS
-#define PRCR_DEC_WORKGROUPS 1024
+#define PRCR_DEC_WORKGROUPS 0    // workgroups per call; 0: as many as are resident at once
+#endif
+#ifndef PRCR_DEC_MFMA
+#define PRCR_DEC_MFMA 1
 #endif
 #ifndef PRCR_DEC_WAVES
 #define PRCR_DEC_WAVES 4
@@ -309,6 +315,366 @@ __global__ __launch_bounds__(kWaves * kWave) void decode_partial_kernel(const De
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 caches: the scores of a tile of 16 keys come from one matrix-core product
+// per 32 elements of the head dim, K(16 keys) x Q(query rows)^T, with float32
+// accumulation.  The float32 query of each head is split into three bf16 parts
+// (the leading 8 significant bits, then the next 8 of what is left, then the
+// rest), whose sum is exactly the float32 value, and the parts are rows of the
+// product, so a key's score is the sum of its three part scores: as exact as a
+// float32 dot product.  The softmax runs once per key in the lanes that hold the
+// key's scores, with a running maximum shared by the wave, and the weights reach
+// the lanes that hold the key's value row through LDS.
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma_16x16x32(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// Orders this wave's LDS writes before its later LDS reads (LDS operations of a
+// wave complete in issue order; this keeps the compiler from moving them).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Part `part` (0, 1, 2) of the three-way bf16 split of x, as bf16 bits in the
+// upper half of a word.  Each part is the truncation of what the previous parts
+// left, and every difference is exact in float32, so the parts sum to x.
+__device__ __forceinline__ uint32_t split_part(float x, int part) {
+  const uint32_t hi = __float_as_uint(x) & 0xFFFF0000u;
+  const float r1 = x - __uint_as_float(hi);
+  const uint32_t mid = __float_as_uint(r1) & 0xFFFF0000u;
+  const float r2 = r1 - __uint_as_float(mid);
+  return part == 0 ? hi : (part == 1 ? mid : __float_as_uint(r2));
+}
+
+// Maximum over the 16 lanes of a DPP row; every lane of the row ends with it.
+__device__ __forceinline__ float row_max16(float s) {
+  s = fmaxf(s, dpp<0xB1>(s));
+  s = fmaxf(s, dpp<0x4E>(s));
+  s = fmaxf(s, dpp<0x141>(s));
+  s = fmaxf(s, dpp<0x140>(s));
+  return s;
+}
+
+// kTileBlocks (paged only): block_size is a multiple of 16, so that every tile
+// of 16 keys (tiles start at multiples of 16) lies in one block.
+template <int D, int GT, bool kPaged, bool kTileBlocks>
+__global__ __launch_bounds__(kWaves * kWave, GT >= 8 ? 2 : 3) void decode_partial_bf16_kernel(const DecodeParams p) {
+  constexpr int kTile = 16;                  // keys per wave and tile: the product's N
+  constexpr int KK = D / 32;                 // products over the head dim per query row tile
+  constexpr int kRows = 3 * GT;              // query rows: three parts of every head
+  constexpr int kATiles = (kRows + 15) / 16; // 16-row query tiles
+  constexpr int kXS = kATiles * 16 + 4;      // floats per key in the part-score exchange (padded)
+  constexpr int EPL = 8;                     // value elements per lane (one 16-byte chunk)
+  constexpr int LPK = D / EPL;               // lanes per value row
+  constexpr int KPW = kWave / LPK;           // value rows per load
+  constexpr int VL = kTile / KPW;            // value loads per lane and tile
+  constexpr int kRowBytes = D * 2;
+  constexpr int KPB = kWaves * kTile;        // keys per workgroup per round of tiles
+  constexpr int P = D / 2;
+  static_assert(KK >= 1 && D % 32 == 0 && VL >= 1, "unsupported head_dim");
+  __shared__ __align__(16) float s_q[GT][D];
+  __shared__ __align__(16) float s_x[kWaves][kTile][kXS];
+  __shared__ __align__(16) float s_p[kWaves][kTile][GT];
+  __shared__ float s_m[kWaves][GT];
+  __shared__ float s_l[kWaves][GT];
+  __shared__ float s_o[kWaves][GT][D];
+
+  const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int kt = lane % kTile;               // key of the tile whose scores this lane holds
+  const int kj = lane / kTile;               // 16-byte chunks 4*kk + kj of that key's row
+  const int vr = lane / LPK;                 // value row slot within a load
+  const int vc = lane % LPK;                 // 16-byte chunk of the value row
+  const int G = p.n_q_heads / p.n_kv_heads;
+
+  const int64_t cap = kPaged ? static_cast<int64_t>(p.max_blocks) * p.block_size : p.s_max;
+  int len = p.cache_len[b];
+  if (len < 0 || len > cap) {
+    if (split == 0 && kvh == 0 && threadIdx.x == 0 && p.err != nullptr)
+      atomicOr(p.err, PRCR_DERR_CAPACITY);
+    len = static_cast<int>(min(max(static_cast<int64_t>(len), int64_t{0}), cap));
+  }
+  const int per = (len + p.n_split - 1) / p.n_split;
+  const int chunk = (per + KPB - 1) / KPB * KPB;
+  const int j0 = min(len, split * chunk);
+  const int j1 = min(len, j0 + chunk);
+
+  // Rotated, scaled query of every head of the group (pair i with i + D/2, the
+  // 1-D rotation at p_next), in float32, in LDS.
+  {
+    const double pq = static_cast<double>(p.q_pos[b]);
+    const double qs = static_cast<double>(p.scale) * kLog2e;
+    for (int idx = threadIdx.x; idx < GT * P; idx += kWaves * kWave) {
+      const int g = idx / P, i = idx % P;
+      const int qh = kvh * G + (g < G ? g : 0);
+      const uint16_t *qrow = static_cast<const uint16_t *>(p.q) + (static_cast<int64_t>(b) * p.n_q_heads + qh) * D;
+      double sn, cs;
+      sincos(pq * p.inv_freq[i], &sn, &cs);
+      const double x = __uint_as_float(static_cast<uint32_t>(qrow[i]) << 16);
+      const double xp = __uint_as_float(static_cast<uint32_t>(qrow[i + P]) << 16);
+      s_q[g][i] = static_cast<float>((x * cs - xp * sn) * qs);
+      s_q[g][i + P] = static_cast<float>((xp * cs + x * sn) * qs);
+    }
+  }
+  __syncthreads();
+  // Query operand: row r = 16a + lane%16 of tile a is part r / GT of head r % GT;
+  // the lane's 8 elements of product kk are those of row chunk 4*kk + kj, the
+  // same chunk as the key operand below.
+  u32x4 qa[kATiles][KK];
+#pragma unroll
+  for (int a = 0; a < kATiles; ++a) {
+    const int r = 16 * a + kt;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      u32x4 w = {0u, 0u, 0u, 0u};
+      if (r < kRows) {
+        const int part = r / GT, g = r % GT;
+        const float *src = &s_q[g][8 * (4 * kk + kj)];
+#pragma unroll
+        for (int h = 0; h < 4; ++h)
+          w[h] = (split_part(src[2 * h], part) >> 16) | (split_part(src[2 * h + 1], part) & 0xFFFF0000u);
+      }
+      qa[a][kk] = w;
+    }
+  }
+
+  const int64_t row_base = kPaged ? 0
+                                  : ((static_cast<int64_t>(b) * p.n_layers + p.layer) * p.n_kv_heads + kvh) * p.s_max;
+  const int64_t row_any = kPaged ? static_cast<int64_t>(p.layer) * p.n_blocks * p.block_size * p.n_kv_heads + kvh
+                                 : row_base;
+  int bad_block = 0;
+  // Block-table entry of key j (the sequence's first entry past the chunk).
+  auto table = [&](int j) -> int32_t {
+    const int js = j < j1 ? j : 0;
+    const int lb = p.block_shift >= 0 ? (js >> p.block_shift) : js / p.block_size;
+    return p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
+  };
+  // Addressing.  Contiguous caches and whole-tile blocks address a tile by its
+  // first row and the stride between its keys' rows (1 row, or n_kv_heads rows
+  // within a block); other paged caches read a block-table entry per key.  Keys
+  // at or past `lim`, or in a block outside the pool, read row_any instead (every
+  // load is issued unconditionally) and are marked dead: they get no weight,
+  // and their values are taken as zero.
+  struct TileAddr {
+    int64_t base;
+    bool ok;
+  };
+  auto tile_addr = [&](int tb, int32_t blk) -> TileAddr {
+    if constexpr (kTileBlocks) {
+      const int lb = p.block_shift >= 0 ? (tb >> p.block_shift) : tb / p.block_size;
+      const bool ok = blk >= 0 && blk < p.n_blocks;
+      return {((static_cast<int64_t>(p.layer) * p.n_blocks + blk) * p.block_size + (tb - lb * p.block_size)) *
+                      p.n_kv_heads + kvh, ok};
+    } else {
+      return {row_base + tb, true};
+    }
+  };
+  constexpr int kStrideHeads = kPaged ? 1 : 0;   // rows between keys: n_kv_heads (paged) or 1
+  auto key_row = [&](int tb, const TileAddr &ta, int t, int lim, bool &live) -> int64_t {
+    const int j = tb + t;
+    const bool in = j < lim;
+    if constexpr (kPaged && !kTileBlocks) {
+      const int32_t blk = table(j);
+      const bool ok = blk >= 0 && blk < p.n_blocks;
+      bad_block |= in && !ok;
+      live = in && ok;
+      const int lb = p.block_shift >= 0 ? (j >> p.block_shift) : j / p.block_size;
+      const int64_t row = ((static_cast<int64_t>(p.layer) * p.n_blocks + blk) * p.block_size + (j - lb * p.block_size)) *
+                              p.n_kv_heads + kvh;
+      return live ? row : row_any;
+    } else {
+      bad_block |= in && !ta.ok;
+      live = in && ta.ok;
+      const int64_t row = ta.base + static_cast<int64_t>(t) * (kStrideHeads ? p.n_kv_heads : 1);
+      return live ? row : row_any;
+    }
+  };
+  // Key rows of a tile in the product's operand layout.  A load reads a quarter
+  // of each of 16 rows and the other quarters follow at once from the same cache
+  // lines, so these are plain loads: as non-temporal loads they took 10 % longer.
+  auto load_k = [&](int tb, const TileAddr &ta, int lim, u32x4 *kd, bool &kl) {
+    const int64_t rk = key_row(tb, ta, kt, lim, kl);
+    const char *kp = static_cast<const char *>(p.cache_k) + rk * kRowBytes + kj * 16;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+      kd[kk] = *reinterpret_cast<const u32x4 *>(kp + kk * 64);
+  };
+  // Value rows of a tile, 16 lanes to a row.
+  auto load_v = [&](int tb, const TileAddr &ta, int lim, u32x4 *vd, bool *vl) {
+    int64_t rv[VL];
+#pragma unroll
+    for (int u = 0; u < VL; ++u) rv[u] = key_row(tb, ta, KPW * u + vr, lim, vl[u]);
+#pragma unroll
+    for (int u = 0; u < VL; ++u)
+      vd[u] = load_nt(static_cast<const char *>(p.cache_v) + rv[u] * kRowBytes + vc * 16);
+  };
+
+  float o[GT][EPL], lsum[GT], mrun[GT];
+#pragma unroll
+  for (int g = 0; g < GT; ++g) {
+    lsum[g] = 0.f;
+    mrun[g] = -FLT_MAX;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) o[g][e] = 0.f;
+  }
+
+  // The wave's tiles start at jw + n*KPB.  With whole-tile blocks the wave reads
+  // the block-table entries of 64 tiles at once, one per lane, and takes each
+  // from its lane when the tile comes; the keys of the next 64 tiles are then a
+  // new round (its first tile loaded again; keys from `lim` on are dead here).
+  //
+  // One buffer per operand, software-pipelined: the next tile's key rows are
+  // loaded once this tile's product has read them, and its value rows once this
+  // tile's weighted sum has; each load's latency hides behind the other half of
+  // a tile's work, and every wait is for the oldest loads only.
+  const int jw = j0 + wave * kTile;
+  // Rounds of 64 tiles with whole-tile blocks; one round otherwise (lim = j1).
+  const int n_tiles = jw < j1 ? (j1 - jw + KPB - 1) / KPB : 0;
+  const int rounds = kTileBlocks ? (n_tiles + kWave - 1) / kWave : (n_tiles > 0 ? 1 : 0);
+  for (int r = 0; r < rounds; ++r) {
+    const int n0 = r * kWave;
+    int32_t tab_lane = 0;
+    if constexpr (kTileBlocks) tab_lane = table(jw + (n0 + lane) * KPB);
+    const int lim = kTileBlocks ? static_cast<int>(min(static_cast<int64_t>(j1),
+                                                       static_cast<int64_t>(jw) + static_cast<int64_t>(n0 + kWave) * KPB))
+                                : j1;
+    auto addr_of = [&](int n) -> TileAddr {
+      const int tb = jw + n * KPB;
+      int32_t blk = 0;
+      if constexpr (kTileBlocks) blk = __builtin_amdgcn_readlane(tab_lane, min(n - n0, kWave - 1));
+      return tile_addr(tb, blk);
+    };
+    u32x4 kr[KK], vv[VL];
+    bool kl, vl[VL];
+    int n = n0, jt = jw + n0 * KPB;
+    TileAddr ta = addr_of(n);
+    load_k(jt, ta, lim, kr, kl);
+    load_v(jt, ta, lim, vv, vl);
+    while (jt < lim) {
+      const TileAddr ta_n = addr_of(n + 1);
+      // Part scores: lane holds rows 16a + 4*(lane/16) + i of the product for key kt.
+      f32x4 acc[kATiles];
+#pragma unroll
+      for (int a = 0; a < kATiles; ++a) {
+        acc[a] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) acc[a] = mfma_16x16x32(qa[a][kk], kr[kk], acc[a]);
+      }
+      bool kl_n;
+      load_k(jt + KPB, ta_n, lim, kr, kl_n);
+#pragma unroll
+      for (int a = 0; a < kATiles; ++a) {
+        const int r0 = 16 * a + 4 * kj;
+        if (r0 < kRows) *reinterpret_cast<f32x4 *>(&s_x[wave][kt][r0]) = acc[a];
+      }
+      wave_lds_sync();
+      // Every row of 16 lanes now takes the same 16 keys: lane kt's key, all heads.
+      float sc[GT];
+      bool rise = false;
+#pragma unroll
+      for (int g = 0; g < GT; ++g) {
+        const float s = (s_x[wave][kt][g] + s_x[wave][kt][GT + g]) + s_x[wave][kt][2 * GT + g];
+        sc[g] = kl ? s : -FLT_MAX;
+        rise = rise || sc[g] > mrun[g];
+      }
+      // The tile's maxima are needed only when some score rose above the running
+      // maximum of its head (rarely, after the first tiles).
+      if (__any(rise)) {
+#pragma unroll
+        for (int g = 0; g < GT; ++g) {
+          const float tmax = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(row_max16(sc[g]))));
+          const float mnew = fmaxf(mrun[g], tmax);
+          const float corr = exp2_fast(mrun[g] - mnew);
+          lsum[g] *= corr;
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) o[g][e] *= corr;
+          mrun[g] = mnew;
+        }
+      }
+      float pw[GT];
+#pragma unroll
+      for (int g = 0; g < GT; ++g) {
+        pw[g] = exp2_fast(sc[g] - mrun[g]);
+        lsum[g] += pw[g];
+      }
+      if (lane < kTile) {
+#pragma unroll
+        for (int g = 0; g < GT; ++g) s_p[wave][kt][g] = pw[g];
+      }
+      wave_lds_sync();
+      // A zero weight times a value read from another row could make a NaN:
+      // values of keys without weight are taken as zero.
+#pragma unroll
+      for (int u = 0; u < VL; ++u) {
+        const int tk = KPW * u + vr;
+        float v[EPL];
+        Elems<uint16_t>::unpack(vl[u] ? vv[u] : u32x4{0u, 0u, 0u, 0u}, v);
+#pragma unroll
+        for (int g = 0; g < GT; ++g) {
+          const float w = s_p[wave][tk][g];
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) o[g][e] = fmaf(w, v[e], o[g][e]);
+        }
+      }
+      load_v(jt + KPB, ta_n, lim, vv, vl);
+      kl = kl_n;
+      jt += KPB;
+      ++n;
+    }
+  }
+  if (bad_block && p.err != nullptr) atomicOr(p.err, PRCR_DERR_BLOCK);
+
+  // Every lane of the wave used the same running maxima: the value row slots add
+  // up plainly, and so do the weight sums of the 16 keys of a row of lanes.
+#pragma unroll
+  for (int off = LPK; off < kWave; off <<= 1) {
+#pragma unroll
+    for (int g = 0; g < GT; ++g) {
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) o[g][e] += __shfl_xor(o[g][e], off);
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < GT; ++g) lsum[g] = group_sum<16>(lsum[g]);
+  if (lane < LPK) {
+#pragma unroll
+    for (int g = 0; g < GT; ++g) {
+      if (lane == 0) {
+        s_m[wave][g] = mrun[g];
+        s_l[wave][g] = lsum[g];
+      }
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) s_o[wave][g][vc * EPL + e] = o[g][e];
+    }
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < G * D; idx += kWaves * kWave) {
+    const int g = idx / D, d = idx % D;
+    float M = -FLT_MAX;
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][g]);
+    float Ls = 0.f, Os = 0.f;
+    for (int w = 0; w < kWaves; ++w) {
+      const float wt = exp2_fast(s_m[w][g] - M);
+      Ls += s_l[w][g] * wt;
+      Os += s_o[w][g][d] * wt;
+    }
+    float *ws = p.ws + ((static_cast<int64_t>(b) * p.n_q_heads + kvh * G + g) * p.n_split + split) * (D + 2);
+    ws[d] = Os;
+    if (d == 0) {
+      ws[D] = M;
+      ws[D + 1] = Ls;
+    }
+  }
+}
+
 // Merge of one query head's split partials.  Each split's (max, sum) is read by
 // one thread, D splits at a time, so that the reads go out together instead of
 // one after another's use; the weights pass through LDS, and every thread then
@@ -371,8 +737,19 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(const DecodeParams p)
 
 template <typename T, int D, int GT, bool kPaged>
 hipError_t launch_split(const DecodeParams &p, hipStream_t stream) {
-  decode_partial_kernel<T, D, GT, kPaged>
-      <<<dim3(p.n_split, p.n_kv_heads, p.batch), kWaves * kWave, 0, stream>>>(p);
+  const dim3 grid(p.n_split, p.n_kv_heads, p.batch);
+  if constexpr (std::is_same_v<T, uint16_t> && PRCR_DEC_MFMA) {
+    if constexpr (kPaged) {
+      if (p.block_size % 16 == 0)
+        decode_partial_bf16_kernel<D, GT, true, true><<<grid, kWaves * kWave, 0, stream>>>(p);
+      else
+        decode_partial_bf16_kernel<D, GT, true, false><<<grid, kWaves * kWave, 0, stream>>>(p);
+    } else {
+      decode_partial_bf16_kernel<D, GT, false, false><<<grid, kWaves * kWave, 0, stream>>>(p);
+    }
+  } else
+    decode_partial_kernel<T, D, GT, kPaged>
+        <<<dim3(p.n_split, p.n_kv_heads, p.batch), kWaves * kWave, 0, stream>>>(p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   decode_combine_kernel<D><<<dim3(p.n_q_heads, p.batch), D, 0, stream>>>(p);
@@ -396,11 +773,15 @@ hipError_t dispatch_dim(const DecodeParams &p, int head_dim, int G, hipStream_t 
 
 }  // namespace
 
-int decode_splits(int64_t capacity, int batch, int n_kv_heads) {
-  // About PRCR_DEC_WORKGROUPS workgroups over the whole batch, and no split of
-  // fewer than 64 keys at full capacity.
+int decode_splits(int64_t capacity, int batch, int n_kv_heads, int group) {
+  // About as many workgroups as the chip holds at once, so that all of them
+  // start together and none waits for a second round: 256 compute units with 3
+  // workgroups of the bf16 kernel each (2 with 8 query heads per KV head, whose
+  // kernel holds more registers).  No split of fewer than 64 keys at full
+  // capacity.
+  const int64_t target = PRCR_DEC_WORKGROUPS > 0 ? PRCR_DEC_WORKGROUPS : (group > 4 ? 512 : 768);
   const int64_t pairs = static_cast<int64_t>(batch) * n_kv_heads;
-  int64_t ns = (PRCR_DEC_WORKGROUPS + pairs - 1) / pairs;
+  int64_t ns = (target + pairs - 1) / pairs;
   const int64_t most = (capacity + 63) / 64;
   if (ns > most) ns = most;
   if (ns < 1) ns = 1;

@@ -159,7 +159,7 @@ hipError_t launch_prefill(const PrefillParams &p, prcr_dtype dtype, int head_dim
                           bool paged, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams &p, prcr_dtype dtype, int head_dim, bool paged,
                          hipStream_t stream);
-int decode_splits(int64_t capacity, int batch, int n_kv_heads);
+int decode_splits(int64_t capacity, int batch, int n_kv_heads, int group);
 
 // A launcher's own refusal of a grid too large for one dispatch is a size error
 // found before any HIP call (PRCR_ERR_SHAPE); anything else the runtime reports

@@ -32,7 +32,7 @@ hipError_t launch_prefill(const PrefillParams &p, prcr_dtype, int, AxisMapId, bo
 hipError_t launch_decode(const DecodeParams &p, prcr_dtype, int, bool, hipStream_t) {
   ++g_calls; g_decode = p; return hipErrorInvalidValue;     // a launch failure maps to PRCR_ERR_HIP
 }
-int decode_splits(int64_t, int, int) { return 3; }
+int decode_splits(int64_t, int, int, int) { return 3; }
 }  // namespace prcr
 
 using namespace prcr;
