@@ -661,17 +661,22 @@ def decode_attention_bw(dev, steps=20, cfg=3):
     mean_s = sum(ms) / len(ms) / 1e3
     nbytes = int(lens.sum()) * w.H * w.D * 2 * 2 + w.B * Hq * w.D * (2 + 4)
     # The same K and V reads with no arithmetic (copyref decode_read_kernel), on the
-    # same cache, with the decode kernel's split and lane layout.
+    # same cache, with the decode kernel's split and lane layout, one layer per call
+    # in the same order as above.
     L = copyref_lib()
     per_split = w.B * Hq * (w.D + 2) * 4
     n_split = prcr.decode_workspace_bytes(cache, w.B, Hq) // per_split
     sink = torch.empty(w.B * w.H * n_split, dtype=torch.int32, device=dev)
     cc = cache.to_c()
 
+    calls = [0]
+
     def read_pattern():
+        layer = calls[0] % w.NL
+        calls[0] += 1
         rc = L.prcr_copyref_decode_read(cache.k.data_ptr(), cache.v.data_ptr(),
                                         cache.block_table.data_ptr() if w.paged else None,
-                                        cl.data_ptr(), sink.data_ptr(), w.B, w.NL, w.H, 0,
+                                        cl.data_ptr(), sink.data_ptr(), w.B, w.NL, w.H, layer,
                                         cc.s_max, cc.block_size, cc.max_blocks, cc.n_blocks,
                                         n_split, int(w.paged), s.cuda_stream)
         if rc != 0:

@@ -5,10 +5,9 @@
 //   prcr_copyref_stream   src -> dst, each workgroup owning one contiguous chunk:
 //                         the attainable read + write rate of the GPU.
 //   prcr_copyref_decode_read  decode attention's reads with no arithmetic: every K and
-//                         V row of one layer's attended slots, with the decode
-//                         kernel's split of each sequence over workgroups, lane
-//                         layout (16 lanes per 256-byte row) and two rows per lane
-//                         group in flight.
+//                         V row of one layer's attended slots, with the bf16
+//                         decode kernel's split of each sequence over workgroups,
+//                         tiles, lane layouts and loads in flight.
 //   prcr_copyref_prefill  prefill capture's access pattern with no arithmetic: one
 //                         layer's raw K/V rows of every prompt token to the
 //                         contiguous cache at slot s, and visual tokens' rows to the
@@ -24,7 +23,8 @@
 //                         batch in flight) and dispatch order (token fastest, then
 //                         row group, then the key array before the value array).
 //
-// Both use 16-byte non-temporal loads and stores, as the rebind does.  Offsets
+// They use 16-byte non-temporal loads and stores, as the rebind does (the decode
+// read's key loads are plain, as in the decode kernel).  Offsets
 // are byte offsets computed by the caller, who checks them against the arrays.
 #include <hip/hip_runtime.h>
 
@@ -149,64 +149,93 @@ struct DecodeReadParams {
   int32_t n_layers, n_kv_heads, layer, s_max, block_size, max_blocks, n_blocks, n_split, paged;
 };
 
-// One workgroup per (split, KV head, sequence), as the decode kernel launches them.
-// Rows are 256 bytes (head_dim 128, bf16): 16 lanes per row, 4 rows per wave and
-// 16 per workgroup per pass, two passes' rows in flight, loads of a batch issued
-// unconditionally (a row past the chunk reads the head's first row, as in the
-// decode kernel).  The words read are folded into one value per workgroup so that
-// the loads are kept.
+// One workgroup per (split, KV head, sequence), as the decode kernel launches them,
+// with the bf16 decode kernel's accesses.  Rows are 256 bytes (head_dim 128, bf16).
+// The sequence's keys are split in whole rounds of 64 keys; a wave takes tiles of
+// 16 keys 64 keys apart.  Key rows are read in the matrix-product operand layout
+// (lane l: row l % 16, 16-byte chunks l / 16 + 4 * kk, plain loads), value rows 16
+// lanes to a row (non-temporal loads); one buffer of each, the next tile's keys
+// loaded once this tile's keys are used and its values once this tile's values
+// are.  Paged caches whose blocks are whole tiles take one block-table entry per
+// tile from a per-wave register filled 64 tiles at a time; others read an entry
+// per key.  Keys past the chunk (or in a block outside the pool) read the head's
+// first row, as in the decode kernel.  The words read are folded into one value
+// per workgroup so that the loads are kept.
+template <bool kPaged, bool kTileBlocks>
 __global__ __launch_bounds__(kThreads) void decode_read_kernel(const DecodeReadParams p) {
-  constexpr int kRowBytes = 256, kLanesPerRow = 16, kRowsPerWg = 16, kIters = 2;
+  constexpr int kRowBytes = 256, kTile = 16, KPB = 64, KK = 4, VL = 4, KPW = 4;
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int grp = wave * (64 / kLanesPerRow) + lane / kLanesPerRow;
-  const int c = lane % kLanesPerRow;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int kt = lane % kTile, kj = lane / kTile;
+  const int vr = lane / 16, vc = lane % 16;
   // lengths clamped to the capacity, and block-table entries outside the pool
   // read the head's first row instead, as in the decode kernel: every access stays
   // inside the arrays whatever the inputs
-  const int64_t cap = p.paged ? static_cast<int64_t>(p.max_blocks) * p.block_size : p.s_max;
+  const int64_t cap = kPaged ? static_cast<int64_t>(p.max_blocks) * p.block_size : p.s_max;
   const int len = static_cast<int>(min(max(static_cast<int64_t>(p.len[b]), int64_t{0}), cap));
   const int per = (len + p.n_split - 1) / p.n_split;
-  const int chunk = (per + kRowsPerWg - 1) / kRowsPerWg * kRowsPerWg;
+  const int chunk = (per + KPB - 1) / KPB * KPB;
   const int j0 = min(len, split * chunk), j1 = min(len, j0 + chunk);
   const int64_t row_base =
-      p.paged ? 0 : ((static_cast<int64_t>(b) * p.n_layers + p.layer) * p.n_kv_heads + kvh) * p.s_max;
+      kPaged ? 0 : ((static_cast<int64_t>(b) * p.n_layers + p.layer) * p.n_kv_heads + kvh) * p.s_max;
   const int64_t row_any =
-      p.paged ? static_cast<int64_t>(p.layer) * p.n_blocks * p.block_size * p.n_kv_heads + kvh : row_base;
-  uint32_t acc = 0;
-  auto load = [&](int jb, u32x4 *kd, u32x4 *vd) {
-    int64_t rows[kIters];
-#pragma unroll
-    for (int u = 0; u < kIters; ++u) {
-      const int j = jb + u * kRowsPerWg + grp;
-      int64_t row = row_base + j;
-      if (p.paged) {
-        const int js = j < j1 ? j : 0;
-        const int lb = js / p.block_size;
-        const int blk = p.block_table[static_cast<int64_t>(b) * p.max_blocks + lb];
-        row = blk >= 0 && blk < p.n_blocks
-                  ? ((static_cast<int64_t>(p.layer) * p.n_blocks + blk) * p.block_size +
-                     (js - lb * p.block_size)) * p.n_kv_heads + kvh
-                  : row_any;
-      }
-      rows[u] = j < j1 ? row : row_any;
-    }
-#pragma unroll
-    for (int u = 0; u < kIters; ++u) {
-      kd[u] = ld(p.k + rows[u] * kRowBytes + c * 16);
-      vd[u] = ld(p.v + rows[u] * kRowBytes + c * 16);
+      kPaged ? static_cast<int64_t>(p.layer) * p.n_blocks * p.block_size * p.n_kv_heads + kvh : row_base;
+  auto table = [&](int j) -> int32_t {
+    const int js = j < j1 ? j : 0;
+    return p.block_table[static_cast<int64_t>(b) * p.max_blocks + js / p.block_size];
+  };
+  // Rows selected without branches, as in the decode kernel.
+  auto row_of = [&](int tb, int j, int lim, int32_t tile_blk) -> int64_t {
+    if constexpr (!kPaged) {
+      return j < lim ? row_base + j : row_any;
+    } else {
+      const int32_t blk = kTileBlocks ? tile_blk : table(j);
+      const int off = kTileBlocks ? (tb % p.block_size) + (j - tb) : j % p.block_size;
+      const int64_t row =
+          ((static_cast<int64_t>(p.layer) * p.n_blocks + blk) * p.block_size + off) * p.n_kv_heads + kvh;
+      return j < lim && blk >= 0 && blk < p.n_blocks ? row : row_any;
     }
   };
-  u32x4 kc[kIters], vc[kIters];
-  load(j0, kc, vc);
-  for (int jb = j0; jb < j1; jb += kRowsPerWg * kIters) {
-    u32x4 nk[kIters], nv[kIters];
-    load(jb + kRowsPerWg * kIters, nk, nv);
+  uint32_t acc = 0;
+  const int jw = j0 + wave * kTile;
+  const int n_tiles = jw < j1 ? (j1 - jw + KPB - 1) / KPB : 0;
+  const int rounds = kTileBlocks ? (n_tiles + 63) / 64 : (n_tiles > 0 ? 1 : 0);
+  for (int r = 0; r < rounds; ++r) {
+    const int n0 = r * 64;
+    int32_t tab = 0;
+    if constexpr (kTileBlocks) tab = table(jw + (n0 + lane) * KPB);
+    const int lim = kTileBlocks ? static_cast<int>(min(static_cast<int64_t>(j1),
+                                                       static_cast<int64_t>(jw) + static_cast<int64_t>(n0 + 64) * KPB))
+                                : j1;
+    auto blk_of = [&](int n) -> int32_t {
+      if constexpr (kTileBlocks) return __builtin_amdgcn_readlane(tab, min(n - n0, 63));
+      return 0;
+    };
+    auto load_k = [&](int tb, int32_t blk, u32x4 *kd) {
+      const char *kp = p.k + row_of(tb, tb + kt, lim, blk) * kRowBytes + kj * 16;
 #pragma unroll
-    for (int u = 0; u < kIters; ++u) {
-      acc ^= kc[u].x ^ kc[u].y ^ kc[u].z ^ kc[u].w ^ vc[u].x ^ vc[u].y ^ vc[u].z ^ vc[u].w;
-      kc[u] = nk[u];
-      vc[u] = nv[u];
+      for (int kk = 0; kk < KK; ++kk) kd[kk] = *reinterpret_cast<const u32x4 *>(kp + kk * 64);
+    };
+    auto load_v = [&](int tb, int32_t blk, u32x4 *vd) {
+#pragma unroll
+      for (int u = 0; u < VL; ++u) vd[u] = ld(p.v + row_of(tb, tb + KPW * u + vr, lim, blk) * kRowBytes + vc * 16);
+    };
+    u32x4 kr[KK], vv[VL];
+    int n = n0, jt = jw + n0 * KPB;
+    int32_t blk = blk_of(n);
+    load_k(jt, blk, kr);
+    load_v(jt, blk, vv);
+    while (jt < lim) {
+      const int32_t blk_n = blk_of(n + 1);
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) acc ^= kr[kk].x ^ kr[kk].y ^ kr[kk].z ^ kr[kk].w;
+      load_k(jt + KPB, blk_n, kr);
+#pragma unroll
+      for (int u = 0; u < VL; ++u) acc ^= vv[u].x ^ vv[u].y ^ vv[u].z ^ vv[u].w;
+      load_v(jt + KPB, blk_n, vv);
+      jt += KPB;
+      ++n;
     }
   }
   for (int o = 32; o > 0; o >>= 1) acc ^= __shfl_xor(acc, o);
@@ -334,7 +363,13 @@ int prcr_copyref_decode_read(const void *k, const void *v, const int32_t *block_
   p.n_blocks = n_blocks;
   p.n_split = n_split;
   p.paged = paged;
-  decode_read_kernel<<<dim3(n_split, n_kv_heads, batch), dim3(kThreads), 0, stream>>>(p);
+  const dim3 grid(n_split, n_kv_heads, batch);
+  if (!paged)
+    decode_read_kernel<false, false><<<grid, dim3(kThreads), 0, stream>>>(p);
+  else if (block_size % 16 == 0)
+    decode_read_kernel<true, true><<<grid, dim3(kThreads), 0, stream>>>(p);
+  else
+    decode_read_kernel<true, false><<<grid, dim3(kThreads), 0, stream>>>(p);
   return hipGetLastError() == hipSuccess ? 0 : 3;
 }
 
