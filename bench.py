@@ -469,8 +469,12 @@ def store_raw_bw(dev, steps=20):
     B, M, S, NL, H, D = 32, 2048, 2560, 36, 8, 128
     g = torch.Generator(device=dev)
     g.manual_seed(3500)
-    raw_k = torch.randn((B, S, H, D), generator=g, device=dev).to(torch.bfloat16)
-    raw_v = torch.randn((B, S, H, D), generator=g, device=dev).to(torch.bfloat16)
+    # Successive calls read different projections (three sets, 1 GB), as successive
+    # layers do: the 268 MB of rows one call reads would otherwise be partly served
+    # from the device's last-level cache on the next call.
+    raws = [(torch.randn((B, S, H, D), generator=g, device=dev).to(torch.bfloat16),
+             torch.randn((B, S, H, D), generator=g, device=dev).to(torch.bfloat16))
+            for _ in range(3)]
     mem = prcr.Memory(torch.empty((B, M, NL, H, D), dtype=torch.bfloat16, device=dev),
                       torch.empty((B, M, NL, H, D), dtype=torch.bfloat16, device=dev),
                       torch.zeros((B, M, 3), dtype=torch.int32, device=dev),
@@ -481,12 +485,12 @@ def store_raw_bw(dev, steps=20):
     torch.cuda.synchronize()
     with torch.cuda.stream(s):
         for layer in range(3):
-            prcr.store_raw(mem, layer, raw_k, raw_v, vis, err, s)
+            prcr.store_raw(mem, layer, *raws[layer % 3], vis, err, s)
         evs = []
         for i in range(steps):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(s)
-            prcr.store_raw(mem, i % NL, raw_k, raw_v, vis, err, s)
+            prcr.store_raw(mem, i % NL, *raws[i % 3], vis, err, s)
             b.record(s)
             evs.append((a, b))
         torch.cuda.synchronize()
@@ -494,7 +498,7 @@ def store_raw_bw(dev, steps=20):
         raise RuntimeError("device reported a data error in the store_raw runs")
     mean_s = sum(a.elapsed_time(b) for a, b in evs) / len(evs) / 1e3
     nbytes = B * M * H * D * 2 * 4
-    del mem, raw_k, raw_v
+    del mem, raws
     torch.cuda.empty_cache()
     return {"kernel": "prcr_store_raw", "workload": f"{B} prompts x {S} rows ({M} visual), {NL} "
             f"layers x {H} KV heads, d {D}, bf16, one layer per call",
