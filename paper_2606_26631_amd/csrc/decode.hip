@@ -679,15 +679,21 @@ __global__ __launch_bounds__(kWaves * kWave, GT >= 8 ? 2 : 3) void decode_partia
 // one thread, D splits at a time, so that the reads go out together instead of
 // one after another's use; the weights pass through LDS, and every thread then
 // accumulates its feature over the splits in split order with the same fused
-// multiply-adds as a sequential merge (an empty split adds exact zeros).
+// multiply-adds as a sequential merge (an empty split adds exact zeros).  The
+// feature values of the first kPre splits do not depend on the weights: they are
+// read in the same round as the (max, sum) pairs.
 template <int D>
 __global__ __launch_bounds__(D) void decode_combine_kernel(const DecodeParams p) {
+  constexpr int kPre = 8;
   __shared__ float s_red[D / kWave];
   __shared__ float s_w[D], s_l[D];
   const int qh = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
   const int lane = d & (kWave - 1), wave = d / kWave;
   const int ns = p.n_split;
   const float *ws = p.ws + (static_cast<int64_t>(b) * p.n_q_heads + qh) * ns * (D + 2);
+  float o_pre[kPre];
+#pragma unroll
+  for (int k = 0; k < kPre; ++k) o_pre[k] = ws[static_cast<int64_t>(min(k, ns - 1)) * (D + 2) + d];
   // Largest max over the splits that saw a key.  Both values of a split are
   // read before either is used; a thread keeps those of its first split (every
   // split, when n_split <= D) for the second pass.
@@ -726,8 +732,19 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(const DecodeParams p)
     __syncthreads();
     const int cnt = min(D, ns - s0);
     const float *o = ws + static_cast<int64_t>(s0) * (D + 2) + d;
+    int k0 = 0;
+    if (s0 == 0) {
+#pragma unroll
+      for (int k = 0; k < kPre; ++k) {
+        if (k < cnt) {
+          Ls = fmaf(s_l[k], s_w[k], Ls);
+          Os = fmaf(o_pre[k], s_w[k], Os);
+        }
+      }
+      k0 = kPre;
+    }
 #pragma unroll 4
-    for (int k = 0; k < cnt; ++k) {
+    for (int k = k0; k < cnt; ++k) {
       Ls = fmaf(s_l[k], s_w[k], Ls);
       Os = fmaf(o[static_cast<int64_t>(k) * (D + 2)], s_w[k], Os);
     }

@@ -33,7 +33,7 @@ __global__ __launch_bounds__(kWaves * kWave) void store_raw_kernel(const StorePa
   int rows[kTokens];
 #pragma unroll
   for (int t = 0; t < kTokens; ++t)
-    rows[t] = p.vis_rows[static_cast<int64_t>(b) * p.max_visual + min(m0 + t, p.max_visual - 1LL)];
+    rows[t] = p.vis_rows[static_cast<int64_t>(b) * p.max_visual + min(m0 + t, static_cast<int64_t>(p.max_visual) - 1)];
   const int n_vis = min(p.n_visual[b], p.max_visual);
   if (m0 >= n_vis) return;
   const char *raw = static_cast<const char *>(values ? p.raw_v : p.raw_k);
