@@ -12,7 +12,9 @@ Each configuration is checked against the oracle to the parity bar: bit-exact
 positions, slots, lengths and values, keys within the key tolerance.  Decode
 attention gets random configurations of its own (grouped-query ratio, lengths,
 capacity, layout), checked to the decode tolerance, and so does the prefill capture
-(prompt mixes of text and images or video frames, cache offsets, key-only memory)."""
+(prompt mixes of text and images or video frames, cache offsets, key-only memory).  The
+raw-memory store gets random storage types, head dims, counts, source rows and layer
+orders, with every byte of the memory compared."""
 import numpy as np
 import pytest
 import torch
@@ -131,3 +133,56 @@ def test_random_prefill_configuration(seed):
     mem, cache, rope, err = pf.run_gpu(start=start)
     ref_mem, ref_cache, ref_err = pf.run_oracle(start=start)
     _compare(pf, mem, cache, err, ref_mem, ref_cache, ref_err)
+
+
+def _bits(t):
+    a = workloads.as_numpy_storage(t)
+    return a.view(np.uint32) if a.dtype == np.float32 else a
+
+
+@pytest.mark.parametrize("seed", range(9800, 9830))
+def test_random_store_configuration(seed):
+    """prcr_store_raw on a random configuration: storage type, head dim (any whose half
+    row is whole 16-byte chunks), head, sequence, visual-token and layer counts, ragged
+    counts (zero and full included), repeated and out-of-range source rows, a key-only
+    memory, several layers in a random order.  Every byte of the memory against the
+    oracle."""
+    r = np.random.default_rng(seed)
+    dtype = "f32" if r.integers(2) else "bf16"
+    D = int(r.choice([8, 16, 24, 32, 64, 96, 128] if dtype == "f32" else [16, 32, 64, 96, 128]))
+    H, B, M, NL = int(r.integers(1, 17)), int(r.integers(1, 41)), int(r.integers(1, 81)), int(r.integers(1, 6))
+    S = int(r.integers(1, 2 * M + 2))
+    key_only = bool(r.integers(4) == 0)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    print(f"seed {seed}: store_raw {dtype} D={D} H={H} B={B} M={M} S={S} NL={NL} key_only={key_only}",
+          flush=True)
+    g = torch.Generator().manual_seed(seed)
+    raw_k = torch.randn((B, S, H, D), generator=g).to(tdt)
+    raw_v = torch.randn((B, S, H, D), generator=g).to(tdt)
+    mk = torch.randn((B, M, NL, H, D), generator=g).to(tdt)
+    mv = None if key_only else torch.randn((B, M, NL, H, D), generator=g).to(tdt)
+    vis = r.integers(0, S, (B, M)).astype(np.int32)             # repeats allowed
+    bad = r.random((B, M)) < 0.03
+    vis[bad] = np.where(r.integers(2, size=int(bad.sum())) == 0, -1 - r.integers(0, 5, int(bad.sum())),
+                        S + r.integers(0, 5, int(bad.sum())))
+    nvis = r.integers(0, M + 1, B).astype(np.int32)
+    nvis[r.random(B) < 0.2] = M
+    nvis[r.random(B) < 0.1] = 0
+    layers = [int(x) for x in r.integers(0, NL, int(r.integers(1, 2 * NL + 1)))]
+    mem = prcr.Memory(mk.to(DEV), None if key_only else mv.to(DEV),
+                      torch.zeros((B, M, 3), dtype=torch.int32, device=DEV), to_dev(nvis),
+                      to_dev(np.zeros((B, M), np.int32)) if key_only else None)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    rk, rv, vd = raw_k.to(DEV), raw_v.to(DEV), to_dev(vis)
+    for layer in layers:
+        prcr.store_raw(mem, layer, rk, None if key_only else rv, vd, err=err)
+    torch.cuda.synchronize()
+    ek, ev = _bits(mk), None if key_only else _bits(mv)
+    e_all = 0
+    for layer in layers:
+        ek, ev, e = oracle.store_raw(ek, ev, layer, _bits(raw_k), _bits(raw_v), vis, nvis)
+        e_all |= e
+    assert int(err.item()) == e_all
+    assert np.array_equal(_bits(mem.k), ek)
+    if not key_only:
+        assert np.array_equal(_bits(mem.v), ev)
