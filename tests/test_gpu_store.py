@@ -1,8 +1,8 @@
 """GPU parity of prcr_store_raw (Sec. 3.1, Eq. (6)-(7)) against the oracle's copy.
 
 Every byte of the memory is compared, the rows the call must leave alone included (the
-memory starts from random bytes).  The shapes span rows of 32 B to 8 KB (several rounds
-of a wave's loop), a key-only memory, odd and zero visual-token counts (a wave's second
+memory starts from random bytes).  The shapes span rows of 32 B to 32 KB (up to sixteen
+rounds of a wave's loop), a key-only memory, odd and zero visual-token counts (a wave's second
 token absent), bad source rows, and the 32-prompt prefill workload at full size, whose
 memory is checked whole for sampled sequences.  Each test prints its case before
 touching the GPU.
@@ -43,6 +43,7 @@ CASES = [
     ("bf16", 4, 128, 7, 33, 50, 2, False),  # 1 KB
     ("bf16", 8, 128, 9, 65, 80, 3, False),  # 2 KB
     ("f32", 16, 128, 3, 11, 30, 2, False),  # 8 KB: four rounds of the wave's loop
+    ("f32", 64, 128, 2, 5, 9, 2, False),    # 32 KB: sixteen rounds
     ("bf16", 8, 128, 5, 21, 40, 2, True),   # key-only memory
     ("f32", 2, 96, 4, 7, 12, 1, True),
 ]
