@@ -149,8 +149,8 @@ struct DecodeReadParams {
   int32_t n_layers, n_kv_heads, layer, s_max, block_size, max_blocks, n_blocks, n_split, paged;
 };
 
-// One workgroup per (split, KV head, sequence), as the decode kernel launches them,
-// with the bf16 decode kernel's accesses.  Rows are 256 bytes (head_dim 128, bf16).
+// One workgroup per (split, KV head, sequence), as the decode kernel launches them
+// (sequences taken longest first), with the bf16 decode kernel's accesses.  Rows are 256 bytes (head_dim 128, bf16).
 // The sequence's keys are split in whole rounds of 64 keys; a wave takes tiles of
 // 16 keys 64 keys apart.  Key rows are read in the matrix-product operand layout
 // (lane l: row l % 16, 16-byte chunks l / 16 + 4 * kk, plain loads), value rows 16
@@ -164,8 +164,21 @@ struct DecodeReadParams {
 template <bool kPaged, bool kTileBlocks>
 __global__ __launch_bounds__(kThreads) void decode_read_kernel(const DecodeReadParams p) {
   constexpr int kRowBytes = 256, kTile = 16, KPB = 64, KK = 4, VL = 4, KPW = 4;
-  const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int split = blockIdx.x, kvh = blockIdx.y;
   const int lane = threadIdx.x & 63;
+  // Rows of workgroups go to the sequences longest first, as in the decode kernel.
+  int b = blockIdx.z;
+  if (gridDim.z <= 64) {
+    const int nb = static_cast<int>(gridDim.z);
+    const int mine = lane < nb ? max(p.len[lane], 0) : -1;
+    int rank = 0;
+    for (int i = 0; i < nb; ++i) {
+      const int other = __builtin_amdgcn_readlane(mine, i);
+      rank += (other > mine) || (other == mine && i < lane);
+    }
+    const unsigned long long hit = __ballot(lane < nb && rank == static_cast<int>(blockIdx.z));
+    b = hit ? __ffsll(static_cast<long long>(hit)) - 1 : b;
+  }
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int kt = lane % kTile, kj = lane / kTile;
   const int vr = lane / 16, vc = lane % 16;
