@@ -26,11 +26,14 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kIters = PRCR_PF_ITERS;
 
-// kOneTok: n_kv_heads is a multiple of the rows per iteration, so the RPI-aligned
-// rows of an iteration are heads of one token.  Validity and slot are then
-// uniform across the wave, and one sincos per lane shared by shuffles covers the
-// token.  Otherwise each lane evaluates the E pairs of its own row.
-template <typename T, int D, class Map, bool kPaged, bool kOneTok>
+// kTPI: whole tokens per iteration of RPI rows.  1: n_kv_heads is a multiple of
+// the rows per iteration, so an iteration's rows are heads of one token;
+// validity and slot are then uniform across the wave, and one sincos per lane
+// shared by shuffles covers the token.  2: the rows per iteration are two
+// tokens' heads (n_kv_heads = RPI / 2); the wave evaluates each token's P angles
+// once (one or two per lane, while every lane is active) and shares them by shuffles.
+// 0: each lane evaluates the E pairs of its own row.
+template <typename T, int D, class Map, bool kPaged, int kTPI>
 __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const PrefillParams p) {
   constexpr int P = D / 2;
   constexpr int E = Store<T>::kPerChunk;
@@ -95,8 +98,8 @@ __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const P
   }
   // Per-row rotation: the lane's E frequencies, taken from the lanes that hold
   // them while every lane is still active.
-  double inv[kOneTok ? 1 : E];
-  if constexpr (!kOneTok) {
+  double inv[kTPI == 0 ? E : 1];
+  if constexpr (kTPI == 0) {
 #pragma unroll
     for (int e = 0; e < E; ++e) inv[e] = __shfl(inv_lane, c * E + e);
   }
@@ -104,6 +107,38 @@ __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const P
 #pragma unroll
   for (int u = 0; u < kIters; ++u) {
     const int b = rb[u], s = rs[u], h = rh[u];
+    // Two tokens per iteration: lane l evaluates pair l % P of token (64 j + l) / P
+    // for j < NS (position ids from the first lane of the token's first row), then
+    // each lane gathers its own row's E pairs.
+    double cs_it[kTPI >= 2 ? E : 1], sn_it[kTPI >= 2 ? E : 1];
+    if constexpr (kTPI >= 2) {
+      constexpr int NS = (kTPI * P + kWave - 1) / kWave;
+      constexpr int kLanesPerTok = kWave / kTPI;
+      const int ax = Map::axis(lane % P);
+      double cv[NS], sv[NS];
+#pragma unroll
+      for (int j = 0; j < NS; ++j) {
+        const int tk = min((j * kWave + lane) / P, kTPI - 1);
+        const int src = tk * kLanesPerTok;
+        const int p0 = __shfl(pid[u][0], src), p1 = __shfl(pid[u][1], src), p2 = __shfl(pid[u][2], src);
+        const double pa = ax == 0 ? p0 : (ax == 1 ? p1 : p2);
+        sincos(pa * inv_lane, &sv[j], &cv[j]);
+      }
+      const int tk_me = lane / kLanesPerTok;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int g = tk_me * P + c * E + e;
+        const int src = g % kWave, slot = g / kWave;
+#pragma unroll
+        for (int j = 0; j < NS; ++j) {
+          const double cj = __shfl(cv[j], src), sj = __shfl(sv[j], src);
+          if (slot == j) {
+            cs_it[e] = cj;
+            sn_it[e] = sj;
+          }
+        }
+      }
+    }
     if (inr[u] && (nt[u] < 0 || nt[u] > p.s_src) && s == 0 && h == 0 && c == 0 && p.err)
       atomicOr(p.err, PRCR_DERR_INDEX);
     if (!live[u]) continue;
@@ -134,7 +169,13 @@ __global__ __launch_bounds__(kWaves * kWave) void prefill_capture_kernel(const P
     }
     if (d >= 0) {
       double cs[E], sn[E];
-      if constexpr (kOneTok) {
+      if constexpr (kTPI >= 2) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          cs[e] = cs_it[e];
+          sn[e] = sn_it[e];
+        }
+      } else if constexpr (kTPI == 1) {
         // All rows of this iteration belong to one token: lane i evaluates pair i
         // (mod P) and each lane gathers its E pairs with shuffles.
         const int pair = lane % P;
@@ -204,12 +245,16 @@ hipError_t launch_one(const PrefillParams &p, hipStream_t stream) {
   int64_t blocks = (rows_all + per_block - 1) / per_block;
   if (blocks < 1) blocks = 1;
   if (!grid_fits(blocks, kWaves * kWave)) return hipErrorInvalidConfiguration;
-  if (p.n_kv_heads % RPI == 0)
-    prefill_capture_kernel<T, D, Map, kPaged, true>
-        <<<dim3(static_cast<unsigned>(blocks)), kWaves * kWave, 0, stream>>>(p);
+  constexpr int P = D / 2;
+  const dim3 grid(static_cast<unsigned>(blocks)), block(kWaves * kWave);
+  const int H = p.n_kv_heads;
+  const int tpi = RPI % H == 0 ? RPI / H : 0;
+  if (H % RPI == 0)
+    prefill_capture_kernel<T, D, Map, kPaged, 1><<<grid, block, 0, stream>>>(p);
+  else if (tpi == 2 && 2 * P <= 2 * kWave)
+    prefill_capture_kernel<T, D, Map, kPaged, 2><<<grid, block, 0, stream>>>(p);
   else
-    prefill_capture_kernel<T, D, Map, kPaged, false>
-        <<<dim3(static_cast<unsigned>(blocks)), kWaves * kWave, 0, stream>>>(p);
+    prefill_capture_kernel<T, D, Map, kPaged, 0><<<grid, block, 0, stream>>>(p);
   return hipGetLastError();
 }
 

@@ -127,14 +127,17 @@ def test_prefill_capture_parity(dtype, D, sections, inter, paged):
 @pytest.mark.parametrize("dtype,D,H", [("bf16", 128, 8), ("bf16", 128, 16), ("bf16", 64, 8),
                                         ("bf16", 64, 16), ("f32", 128, 8), ("f32", 64, 12),
                                         ("bf16", 128, 4), ("bf16", 128, 2), ("bf16", 64, 4),
-                                        ("f32", 128, 2), ("bf16", 128, 3), ("bf16", 128, 1)])
+                                        ("f32", 128, 2), ("f32", 64, 4), ("f32", 128, 1),
+                                        ("bf16", 128, 3), ("bf16", 128, 1)])
 @pytest.mark.parametrize("paged", [False, True])
 def test_prefill_head_counts(dtype, D, H, paged):
-    """Head counts on both sides of the kernel's specialisation: when n_kv_heads is a
+    """Head counts on every side of the kernel's specialisation.  When n_kv_heads is a
     multiple of a wave iteration's rows (8 at bf16 d 128 and f32 d 64, 16 at bf16 d 64,
-    4 at f32 d 128), an iteration is one token; otherwise its rows span tokens (bf16
-    d 128 with 4, 3, 2 or 1 heads, bf16 d 64 with 8 or 4, f32 d 128 with 2, f32 d 64
-    with 12) and each row evaluates its own angles."""
+    4 at f32 d 128), an iteration is one token.  When it is half of them (bf16 d 128
+    with 4, bf16 d 64 with 8, f32 d 128 with 2, f32 d 64 with 4), an iteration is two
+    tokens whose angles the wave evaluates once each.  Otherwise (bf16 d 128 with 3, 2
+    or 1 heads, bf16 d 64 with 4, f32 d 128 with 1, f32 d 64 with 12) each row
+    evaluates its own angles."""
     sections = (16, 24, 24) if D == 128 else (8, 12, 12)
     pf = Prefill(dtype, D, sections, False, paged, NL=2, H=H, seed=11)
     _say(f"prefill capture {dtype} D={D} H={H} paged={paged}")
