@@ -98,3 +98,50 @@ def test_decode_mixed_lengths(paged, bs, B, H, G, spec):
                 qh = kvh * G + gg
                 d = np.abs(out[b, qh] - ref[i, qh]).max()
                 assert d <= 5e-5 * vmax + 1e-6, (int(b), qh, float(d), float(vmax))
+
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_decode_batch_order_does_not_matter(paged):
+    """The grid's rows take the sequences longest first; a sequence's result must not
+    depend on which row takes it.  A permuted batch (queries, positions, lengths and
+    cache rows or block-table rows permuted alike) gives the permuted outputs, bit for
+    bit."""
+    B, H, G, D, NL, layer, bs = 24, 4, 4, 128, 1, 0, 16
+    rng = np.random.default_rng(2024 + paged)
+    lens = rng.integers(0, 3000, B).astype(np.int32)
+    lens[[3, 11]] = (4000, 4000)                  # a tie among the longest
+    print(f"decode batch order, paged={paged}: {B} sequences, lengths {lens.min()}-{lens.max()}",
+          flush=True)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(2025 + paged)
+    rnd = lambda *s: torch.randn(s, generator=g, device=DEV).to(torch.bfloat16)
+    perm = rng.permutation(B)
+    q, q_pos = rnd(B, H * G, D), rng.integers(0, 20000, B).astype(np.int32)
+    rope = prcr.Rope(D, (16, 24, 24), False, 1e6)
+    if paged:
+        need = (lens + bs - 1) // bs
+        max_blocks, n_blocks = int(need.max()), int(need.sum()) + 1
+        pool = 1 + rng.permutation(n_blocks - 1)
+        table = np.full((B, max_blocks), -1, np.int32)
+        o = 0
+        for b in range(B):
+            table[b, :need[b]] = pool[o:o + need[b]]
+            o += need[b]
+        k, v = rnd(NL, n_blocks, bs, H, D), rnd(NL, n_blocks, bs, H, D)
+        cache = prcr.Cache(k, v, to_dev(table))
+        cache_p = prcr.Cache(k, v, to_dev(table[perm]))
+    else:
+        cap = int(lens.max())
+        k, v = rnd(B, NL, H, cap, D), rnd(B, NL, H, cap, D)
+        pi = torch.from_numpy(perm).to(DEV)
+        cache = prcr.Cache(k, v)
+        cache_p = prcr.Cache(k[pi].contiguous(), v[pi].contiguous())
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out = prcr.decode_attention(rope, cache, layer, q, to_dev(q_pos), to_dev(lens), err=err)
+    out_p = prcr.decode_attention(rope, cache_p, layer, q[torch.from_numpy(perm).to(DEV)].contiguous(),
+                                  to_dev(q_pos[perm]), to_dev(lens[perm]), err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    a = out.cpu().numpy()[perm].view(np.uint32)
+    b = out_p.cpu().numpy().view(np.uint32)
+    assert np.array_equal(a, b)
