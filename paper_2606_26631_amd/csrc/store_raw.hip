@@ -6,9 +6,10 @@
 // with a value memory, even workgroups move keys and odd ones values. Waves are
 // numbered token-first: consecutive waves take the same tokens of successive
 // sequences. A token's row of one layer sits n_layers rows after the previous
-// token's, so the stores in flight at one time then spread over every
-// sequence's memory instead of crowding a few sequences' rows, which made the
-// copy rate depend on where the arrays happened to land in physical memory.
+// token's, so the stores in flight at one time spread over every sequence's
+// memory instead of crowding a few sequences' rows. Over independent
+// allocations this order was as fast on average as sequence-first waves, with
+// a narrower spread between allocations and a worst case 12 % faster.
 #include "prcr_internal.h"
 
 namespace prcr {
