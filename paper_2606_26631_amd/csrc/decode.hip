@@ -7,7 +7,8 @@
 // Split-K flash decoding.  Kernel 1: one workgroup per (key chunk, KV head,
 // sequence) streams its keys and values once for all G query heads of the
 // group, and the sequence's keys are split evenly over its workgroups, about as
-// many workgroups in all as the chip holds at once.  bf16 caches take the
+// many workgroups in all as the chip holds at once (with at most 64 sequences,
+// the grid's sequence rows take the sequences longest first).  bf16 caches take the
 // scores of 16 keys at a time from matrix-core products (decode_partial_bf16_kernel);
 // float32 caches take a 16-byte chunk of a key row per lane with scores reduced
 // across the lanes of a row by DPP lane permutations (decode_partial_kernel).
