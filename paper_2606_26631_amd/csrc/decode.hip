@@ -391,7 +391,7 @@ __global__ __launch_bounds__(kWaves * kWave, GT >= 8 ? 2 : 3) void decode_partia
   constexpr int kRows = 3 * GT;              // query rows: three parts of every head
   constexpr int kATiles = (kRows + 15) / 16; // 16-row query tiles
   constexpr int kXS = kATiles * 16 + 4;      // floats per key in the part-score exchange (padded)
-  constexpr int EPL = 8;                     // value elements per lane (one 16-byte chunk)
+  constexpr int EPL = Elems<uint16_t>::kPerChunk;   // value elements per lane (one 16-byte chunk)
   constexpr int LPK = D / EPL;               // lanes per value row
   constexpr int KPW = kWave / LPK;           // value rows per load
   constexpr int VL = kTile / KPW;            // value loads per lane and tile
