@@ -2,7 +2,9 @@
 //
 // One workgroup per sequence: a block-wide min/max over the valid selected
 // coordinates (Eq. (8)), then one thread per token writes its new (t, h, w)
-// position.  PCR positions are the exact rational of Eq. (9)-(10) over integer
+// position.  The workgroup has 64-1024 threads, as many as the mean selection
+// per sequence needs, so that a typical sequence's tokens are read in one round
+// of loads instead of one round per 256 tokens.  PCR positions are the exact rational of Eq. (9)-(10) over integer
 // numerator and denominator, divided once in double precision, which makes the
 // value the correctly rounded one and identical on every device.
 #include <climits>
@@ -14,8 +16,6 @@
 namespace prcr {
 namespace {
 
-constexpr int kThreads = 256;
-
 __device__ __forceinline__ int wave_min(int v) {
   for (int o = kWave / 2; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
   return v;
@@ -25,6 +25,7 @@ __device__ __forceinline__ int wave_max(int v) {
   return v;
 }
 
+template <int kThreads>
 __global__ __launch_bounds__(kThreads) void reassign_kernel(const ReassignParams p) {
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
@@ -146,8 +147,17 @@ __global__ __launch_bounds__(kThreads) void reassign_kernel(const ReassignParams
 }  // namespace
 
 hipError_t launch_reassign(const ReassignParams &p, hipStream_t stream) {
-  if (!grid_fits(p.batch, kThreads)) return hipErrorInvalidConfiguration;
-  reassign_kernel<<<dim3(p.batch), dim3(kThreads), 0, stream>>>(p);
+  if (!grid_fits(p.batch, 1024)) return hipErrorInvalidConfiguration;
+  const int64_t mean_k = p.batch > 0 ? (static_cast<int64_t>(p.total_k) + p.batch - 1) / p.batch : 0;
+  const dim3 grid(p.batch);
+  if (mean_k <= 64)
+    reassign_kernel<64><<<grid, dim3(64), 0, stream>>>(p);
+  else if (mean_k <= 256)
+    reassign_kernel<256><<<grid, dim3(256), 0, stream>>>(p);
+  else if (mean_k <= 512)
+    reassign_kernel<512><<<grid, dim3(512), 0, stream>>>(p);
+  else
+    reassign_kernel<1024><<<grid, dim3(1024), 0, stream>>>(p);
   return hipGetLastError();
 }
 
