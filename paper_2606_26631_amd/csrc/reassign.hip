@@ -147,17 +147,16 @@ __global__ __launch_bounds__(kThreads) void reassign_kernel(const ReassignParams
 }  // namespace
 
 hipError_t launch_reassign(const ReassignParams &p, hipStream_t stream) {
-  if (!grid_fits(p.batch, 1024)) return hipErrorInvalidConfiguration;
   const int64_t mean_k = p.batch > 0 ? (static_cast<int64_t>(p.total_k) + p.batch - 1) / p.batch : 0;
+  const int threads = mean_k <= 64 ? 64 : (mean_k <= 256 ? 256 : (mean_k <= 512 ? 512 : 1024));
+  if (!grid_fits(p.batch, threads)) return hipErrorInvalidConfiguration;
   const dim3 grid(p.batch);
-  if (mean_k <= 64)
-    reassign_kernel<64><<<grid, dim3(64), 0, stream>>>(p);
-  else if (mean_k <= 256)
-    reassign_kernel<256><<<grid, dim3(256), 0, stream>>>(p);
-  else if (mean_k <= 512)
-    reassign_kernel<512><<<grid, dim3(512), 0, stream>>>(p);
-  else
-    reassign_kernel<1024><<<grid, dim3(1024), 0, stream>>>(p);
+  switch (threads) {
+    case 64: reassign_kernel<64><<<grid, dim3(64), 0, stream>>>(p); break;
+    case 256: reassign_kernel<256><<<grid, dim3(256), 0, stream>>>(p); break;
+    case 512: reassign_kernel<512><<<grid, dim3(512), 0, stream>>>(p); break;
+    default: reassign_kernel<1024><<<grid, dim3(1024), 0, stream>>>(p); break;
+  }
   return hipGetLastError();
 }
 

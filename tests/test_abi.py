@@ -235,13 +235,17 @@ def test_output_aliasing_refused():
 
 @host_only
 def test_grid_limits():
-    # A launch carries each grid extent as a 32-bit count of work-items (256 per
-    # workgroup here).  Problems beyond it are size errors, refused before any HIP
-    # call, so these placeholder pointers are never used.
+    # A launch carries each grid extent as a 32-bit count of work-items.  Problems
+    # beyond it are size errors, refused before any HIP call, so these placeholder
+    # pointers are never used.
     rope, mem, cache = good()
     assert call_rebind(rope, mem, cache, total_k=1 << 25) == 2
-    r2, m2, c2 = good(); m2.batch = 1 << 24                # one workgroup per sequence
+    # reassignment: one workgroup per sequence, 64 threads when at most 64 tokens
+    # per sequence are selected, 256 up to 256
+    r2, m2, c2 = good(); m2.batch = 1 << 26
     assert call_reassign(m2) == 2
+    r2, m2, c2 = good(); m2.batch = 1 << 24
+    assert call_reassign(m2, total_k=65 << 24) == 2
     r2, m2, c2 = good(); m2.max_visual = 1 << 26           # four tokens per workgroup
     assert call_store(m2) == 2
     assert call_prefill(rope, mem, cache, s_src=1 << 27) == 2
