@@ -357,6 +357,27 @@ def test_many_sequences(paged, fused):
     assert_parity(case, gpu, ref)
 
 
+@pytest.mark.parametrize("ks", [
+    (300,) + (1,) * 9,          # mean 31: 64-thread workgroups, the long sequence in 5 rounds
+    (700, 1, 0, 3),             # mean 176: 256 threads, 3 rounds
+    (900, 100),                 # mean 500: 512 threads, 2 rounds
+    (2000, 600),                # mean 1300: 1024 threads, 2 rounds
+])
+def test_reassign_skewed_selections(ks):
+    """The reassignment sizes its workgroup to the mean selection per sequence, so a
+    sequence far above the mean loops over its tokens in several rounds: positions,
+    next positions and the rebound rows against the oracle."""
+    lens = tuple(10 + 3 * i for i in range(len(ks)))
+    w = workloads.custom(B=len(ks), NL=1, H=1, D=64, dtype="f32", sections=(8, 12, 12),
+                         frames=4, gh=24, gw=24, ks=ks, lens=lens, seed=500 + len(ks))
+    _say(f"skewed selections {ks[:4]}..., total_k={w.total_k}")
+    case = Case(w)
+    for fused in (False, True):
+        gpu, ref = run_both(case, w.sel_off, w.sel_idx, w.p_txt, w.cache_len, fused=fused)
+        assert_parity(case, gpu, ref)
+        case = Case(w)
+
+
 @pytest.mark.parametrize("dtype,paged", [("bf16", False), ("bf16", True), ("f32", False)])
 def test_special_values(dtype, paged):
     """NaN, infinities, the largest finite value (whose rotation overflows), the
